@@ -1,0 +1,245 @@
+"""PRECOG reference oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain, sequential fp64 implementations of every operation the GPU path
+computes.  Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` may import this package.  It shares no code with the HIP
+path (``paper_2608_02560_amd``) and neither side imports the other; only the
+seeded input generators (``paper_2608_02560_amd.synth``) serve both.
+
+What each function follows in the paper (arXiv 2608.02560):
+
+* ``scan``        -- Eq. 1 (Sec. 3) rolled over the sequence (the rollout
+  S(h, x_1:T) of App. A), final-state capture of offline indexing (Sec. 4.2)
+  and the gated readout read as (C_t . h_t + Dskip x_t) * silu(z_t).
+* ``top1``        -- cosine top-1 over unit-norm keys (Sec. 4.2, query time).
+* ``gather``      -- state injection h_init <- h^(i*) (Sec. 4.2, query time).
+* ``trajectory``  -- SMC per-step trajectory (Sec. 5.1) thinned by the dial K
+  (Sec. 5.2).
+* ``topk_compose``-- softmax-weighted composition of the top-k states
+  (Sec. 5.4, Eq. smc-fusion; Fig. 1 caption).
+* ``route2``, ``ema`` -- SMC two-stage routing (Sec. 5.1, Eqs. smc-domain,
+  smc-sub) and semantic EMA consolidation (Sec. 5.3, Eq. smc-ema).
+* ``round_bf16``, ``round_f16`` -- round-to-nearest-even storage rounding of
+  fp64 values (the paper stores states at FP16, Sec. 4.2).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "precog_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libprecog_oracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the C oracle with gcc -O2 (no fast-math); returns the .so path."""
+    if force or not os.path.exists(_LIB_PATH) or (
+        os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
+    ):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
+             "-fno-fast-math", "-ffp-contract=off", "-o", tmp, _SRC, "-lm"]
+        )
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        i64, dp, fp, ip = (ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                           ctypes.c_void_p)
+        lib.oracle_scan_f64.argtypes = [i64, i64, i64, i64] + [dp] * 10 + [ctypes.c_int]
+        lib.oracle_scan_f64.restype = ctypes.c_int
+        lib.oracle_trajectory_f64.argtypes = [i64] * 5 + [dp] * 6
+        lib.oracle_trajectory_f64.restype = ctypes.c_int
+        lib.oracle_top1_f64.argtypes = [i64, i64, i64, fp, fp, ip, dp, ctypes.c_int]
+        lib.oracle_top1_f64.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _f64(a):
+    """Exact widening of a numpy array or a torch tensor (any float dtype)."""
+    if a is None:
+        return None
+    if hasattr(a, "detach"):  # torch tensor
+        a = a.detach().cpu().double().numpy()
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def scan(x, dt, A, B, C, z=None, Dskip=None, h0=None, want_y=True,
+         want_hT=True, nthreads=1):
+    """Sequential fp64 selective scan (Eq. 1, Sec. 3).
+
+    Shapes: x, dt, z [Bt, L, D]; A [D, N] (positive: decay exp(-dt*A));
+    B, C [Bt, L, N]; Dskip [D]; h0 [Bt, D, N].  Returns (y, hT) as fp64
+    arrays (either may be None when not requested).
+    """
+    x, dt, A, B, C = (_f64(v) for v in (x, dt, A, B, C))
+    z, Dskip, h0 = _f64(z), _f64(Dskip), _f64(h0)
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    assert A.shape == (D, N) and dt.shape == x.shape
+    assert B.shape == (Bt, L, N)
+    if want_y:
+        assert C is not None and C.shape == (Bt, L, N)
+    if z is not None:
+        assert z.shape == x.shape
+    if Dskip is not None:
+        assert Dskip.shape == (D,)
+    if h0 is not None:
+        assert h0.shape == (Bt, D, N)
+    y = np.zeros((Bt, L, D)) if want_y else None
+    hT = np.zeros((Bt, D, N)) if want_hT else None
+    rc = _load().oracle_scan_f64(Bt, L, D, N, _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
+                                 _ptr(C if want_y else None), _ptr(z), _ptr(Dskip),
+                                 _ptr(h0), _ptr(y), _ptr(hT), int(nthreads))
+    if rc:
+        raise RuntimeError("oracle_scan_f64 failed with code %d" % rc)
+    return y, hT
+
+
+def trajectory(x, dt, A, B, k, h0=None):
+    """States after tokens k, 2k, ... of each row (Sec. 5.1-5.2): [Bt, L//k, D, N]."""
+    x, dt, A, B, h0 = (_f64(v) for v in (x, dt, A, B, h0))
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    out = np.zeros((Bt, L // k, D, N))
+    rc = _load().oracle_trajectory_f64(Bt, L, D, N, int(k), _ptr(x), _ptr(dt),
+                                       _ptr(A), _ptr(B), _ptr(h0), _ptr(out))
+    if rc:
+        raise RuntimeError("oracle_trajectory_f64 failed with code %d" % rc)
+    return out
+
+
+def _f32(a):
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().float().numpy()
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def top1(query, index, nthreads=1):
+    """Exact cosine top-1 (Sec. 4.2): fp64 inner products summed in index
+    order; ties go to the lowest row.  Returns (idx int32 [Q], best fp64 [Q])."""
+    q, K = _f32(query), _f32(index)
+    Q, E = q.shape
+    M = K.shape[0]
+    assert K.shape[1] == E
+    idx = np.empty(Q, np.int32)
+    best = np.empty(Q, np.float64)
+    rc = _load().oracle_top1_f64(Q, M, E, _ptr(q), _ptr(K), _ptr(idx),
+                                 _ptr(best), int(nthreads))
+    if rc:
+        raise RuntimeError("oracle_top1_f64 failed with code %d" % rc)
+    return idx, best
+
+
+def gather(store, idx):
+    """State injection h0[q] = store[idx[q]] (Sec. 4.2 query time), exact fp64."""
+    return _f64(store)[np.asarray(idx, dtype=np.int64)]
+
+
+def topk_scores(query, index, k):
+    """Top-k by fp64 score (products exact, summed in index order), ties to
+    the lower row, best first.  Returns (idx [Q, k] int64, score [Q, k])."""
+    q = _f32(query).astype(np.float64)
+    K = _f32(index).astype(np.float64)
+    Q, E = q.shape
+    M = K.shape[0]
+    idx = np.empty((Q, k), np.int64)
+    sc = np.empty((Q, k))
+    for qi in range(Q):
+        s = np.zeros(M)
+        for e in range(E):  # one sequential sum per row, vectorised over rows
+            s = s + q[qi, e] * K[:, e]
+        order = sorted(range(M), key=lambda i: (-s[i], i))[:k]
+        idx[qi] = order
+        sc[qi] = s[order]
+    return idx, sc
+
+
+def topk_compose(store, idx, scores, tau):
+    """h_init = sum_j w_j h^(j), w = softmax(score / tau) over the k retrieved
+    states (Sec. 5.4, Eq. smc-fusion; composition of Fig. 1).  fp64."""
+    store = _f64(store)
+    Q, k = idx.shape
+    out = np.zeros((Q,) + store.shape[1:])
+    for qi in range(Q):
+        logits = np.asarray(scores[qi], np.float64) / tau
+        m = max(logits)
+        w = [np.exp(v - m) for v in logits]
+        tot = sum(w)
+        for j in range(k):
+            out[qi] += (w[j] / tot) * store[int(idx[qi, j])]
+    return out
+
+
+def route2(emb, domain_protos, sub_protos):
+    """Two-stage routing (Sec. 5.1, Eqs. smc-domain and smc-sub):
+    m* = argmax_m <phi(c), p_m>, then j* = argmax_j <phi(c), q_{m*, j}>.
+    sub_protos: [M, J, E].  Ties go to the lower index.  fp64 sums in order."""
+    e = _f32(emb).astype(np.float64)
+    P = _f32(domain_protos).astype(np.float64)
+    S = _f32(sub_protos).astype(np.float64)
+    out_m = np.empty(e.shape[0], np.int32)
+    out_j = np.empty(e.shape[0], np.int32)
+    for c in range(e.shape[0]):
+        best, bm = None, -1
+        for m in range(P.shape[0]):
+            s = 0.0
+            for k in range(e.shape[1]):
+                s += e[c, k] * P[m, k]
+            if bm < 0 or s > best:
+                best, bm = s, m
+        best, bj = None, -1
+        for j in range(S.shape[1]):
+            s = 0.0
+            for k in range(e.shape[1]):
+                s += e[c, k] * S[bm, j, k]
+            if bj < 0 or s > best:
+                best, bj = s, j
+        out_m[c], out_j[c] = bm, bj
+    return out_m, out_j
+
+
+def ema(state, contribution, alpha):
+    """Semantic consolidation s <- (1 - alpha) s + alpha h (Sec. 5.3, Eq. smc-ema)."""
+    return (1.0 - alpha) * _f64(state) + alpha * _f64(contribution)
+
+
+def round_bf16(a):
+    """Round fp64 values to the nearest bfloat16 value, ties to even
+    (8 significant bits, exponent range of fp32, subnormals kept)."""
+    a = np.asarray(a, dtype=np.float64)
+    _, e = np.frexp(a)
+    q = np.ldexp(1.0, np.maximum(e, -125) - 8)
+    return np.rint(a / q) * q
+
+
+def round_f16(a):
+    """Round fp64 values to the nearest IEEE binary16 value, ties to even
+    (11 significant bits, min normal 2^-14, subnormals kept)."""
+    a = np.asarray(a, dtype=np.float64)
+    _, e = np.frexp(a)
+    q = np.ldexp(1.0, np.maximum(e, -13) - 11)
+    r = np.rint(a / q) * q
+    return np.where(np.abs(r) > 65504.0, np.copysign(np.inf, a), r)
+
+
+def bf16_ulp(a):
+    """Spacing of bfloat16 values at |a| (for one-ulp checks)."""
+    a = np.asarray(a, dtype=np.float64)
+    _, e = np.frexp(a)
+    return np.ldexp(1.0, np.maximum(e, -125) - 8)
