@@ -1,0 +1,275 @@
+"""Benchmark of the PRECOG hot path on one MI355X.
+
+Default workload: corpus-chunk encoding -- 64 chunks x 3000 tokens, D=2048,
+N=16, bf16 inputs, fp32 state, bf16 y, fp16 captured final states -- the
+offline indexing pass of Sec. 4.2.  One step = one precog_scan_encode call
+over the whole batch, inputs resident in HBM.  Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--extra]
+
+--extra also times the query-time path (top-1 retrieval, state injection,
+32-token query prefill), the long-context chunked scan and one layer of the
+large corpus encode, reported under "extra".
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "SSM prefill scan tokens/s & achieved HBM GB/s (fraction of peak), 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+# fp32 vector issue rate without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
+
+
+def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate=True):
+    """Algorithmic bytes of one scan: every input read once, every output
+    written once (x, dt, [z] per (t, d); B, [C] per (t, n); y per (t, d);
+    hT per (d, n); A and Dskip per (d, n) / d)."""
+    td = B * L * D
+    tn = B * L * N
+    total = td * in_bytes * (2 + (1 if (readout and gate) else 0))
+    total += tn * in_bytes * (2 if readout else 1)
+    if readout:
+        total += td * y_bytes + D * 4
+    total += B * D * N * st_bytes + D * N * 4
+    return total
+
+
+def cpu_threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def time_events(fn, reps, flush=None):
+    """Average duration of fn() in ms, HIP events on torch's current stream
+    (the stream every precog call here is enqueued on)."""
+    import torch
+
+    total = 0.0
+    for _ in range(reps):
+        if flush is not None:
+            flush()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn()
+        e.record()
+        e.synchronize()
+        total += s.elapsed_time(e)
+    return total / reps
+
+
+def cpu_baseline_corpus(inp, wl, rows_b):
+    """The oracle, as it stands, on the first rows_b chunks of the workload
+    (all channels, all tokens), timed on the host cores."""
+    import oracle
+
+    nthr = cpu_threads()
+    sub = {k: (v[:rows_b].cpu() if v is not None and v.dim() == 3 else
+               (v.cpu() if v is not None else None)) for k, v in inp.items()}
+    t0 = time.perf_counter()
+    oracle.scan(sub["x"], sub["dt"], sub["A"], sub["B"], sub["C"], sub["z"], sub["Dskip"],
+                None, nthreads=nthr)
+    dt = time.perf_counter() - t0
+    tokens = rows_b * wl.seqlen
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
+            "sample": "%d of %d chunks x %d tokens x %d channels, N=%d, fp64, %.1f s wall"
+                      % (rows_b, wl.batch, wl.seqlen, wl.dim, wl.dstate, dt)}
+
+
+def bench_corpus(args):
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    wl = synth.CORPUS_ENCODE
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, wl.dt_mu, wl.dt_sigma)
+    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((B, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=args.chunk)
+    nws = P.scan_workspace_bytes(desc)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+
+    def step():
+        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], None, y, hT, ws, nws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = start.elapsed_time(end) / args.steps
+    ms = max(wall * 1e3 / args.steps, ev_ms)
+    nbytes = scan_bytes(B, L, D, N)
+    tokens = B * L
+    achieved = nbytes / (ev_ms * 1e-3) / 1e9
+    valu_ops = 5 * B * L * D * N  # mul, exp2, mul, fma, fma per (t, d, n)
+    out = {
+        "metric": METRIC,
+        "value": tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "io_dtypes": "x/dt/z/B/C bf16, y bf16, state fp32, hT fp16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "seqlen": L, "dim": D, "dstate": N,
+                   "chunk": args.chunk or "auto", "parallelism": "single GPU"},
+        "achieved_gbps": achieved,
+        "hbm_frac": achieved / HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "scan_kernel<16, bf16, bf16, fp16, readout>",
+                     "bytes_per_launch": nbytes, "kernel_ms": ev_ms},
+        "alu": {"achieved_ops": valu_ops / (ev_ms * 1e-3), "peak_ops": VALU_PEAK_OPS,
+                "frac": valu_ops / (ev_ms * 1e-3) / VALU_PEAK_OPS,
+                "note": "5 VALU issues per (t,d,n) counted algorithmically"},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline_corpus(inp, wl, args.cpu_rows)
+    del inp, y, hT, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_extra(args):
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    res = {}
+    flush_buf = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
+    flush = lambda: flush_buf.zero_()  # evicts the 256 MB last-level cache
+
+    # query-time path
+    cfg = synth.RETRIEVAL
+    q, K, _, _ = synth.retrieval_inputs_host(cfg["Q"], cfg["M"], cfg["E"], cfg["planted"],
+                                             cfg["seed"])
+    q, K = q.cuda(), K.cuda()
+    wl = synth.QUERY_PREFILL
+    D, N = wl.dim, wl.dstate
+    store = synth.state_store(cfg["M"], D * N, seed=33, device="cuda")
+    idx = torch.empty(cfg["Q"], dtype=torch.int32, device="cuda")
+    nws = P.retrieve_workspace_bytes(cfg["Q"], cfg["M"], cfg["E"])
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    inp = synth.scan_inputs_device(wl.batch, wl.seqlen, D, N, wl.seed, torch.bfloat16)
+    h0 = torch.empty((wl.batch, D, N), dtype=torch.float16, device="cuda")
+    y = torch.empty((wl.batch, wl.seqlen, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((wl.batch, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(wl.batch, wl.seqlen, D, N, P.BF16, P.BF16, P.F16)
+    r_ms = time_events(lambda: P.retrieve_top1(q, K, idx, ws, nws), 20, flush)
+    g_ms = time_events(lambda: P.inject_gather(store, idx, h0.view(wl.batch, -1)), 20, flush)
+    s_ms = time_events(lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"],
+                                             inp["C"], inp["z"], inp["Dskip"], h0, y, hT), 20,
+                       flush)
+
+    def pipeline():
+        P.retrieve_top1(q, K, idx, ws, nws)
+        P.inject_gather(store, idx, h0.view(wl.batch, -1))
+        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], h0, y, hT)
+
+    e_ms = time_events(pipeline, 20, flush)
+    flops = 2.0 * cfg["Q"] * cfg["M"] * cfg["E"]
+    sbytes = scan_bytes(wl.batch, wl.seqlen, D, N) + wl.batch * D * N * 2
+    res["query_path"] = {
+        "workload": "Q=256 over M=10000 x 384 keys; store [10000, 1024, 16] fp16; "
+                    "32-token bf16 query prefill; cold last-level cache",
+        "retrieve_ms": r_ms, "retrieve_tflops": flops / (r_ms * 1e-3) / 1e12,
+        "retrieve_mfma_frac": flops / (r_ms * 1e-3) / 157.3e12,
+        "gather_ms": g_ms, "gather_gbps": 2 * wl.batch * D * N * 2 / (g_ms * 1e-3) / 1e9,
+        "prefill_ms": s_ms, "prefill_gbps": sbytes / (s_ms * 1e-3) / 1e9,
+        "end_to_end_ms": e_ms,
+    }
+    del inp, y, hT, h0, store, ws, q, K
+    torch.cuda.empty_cache()
+
+    # long-context chunked scan (one timed call)
+    wl = synth.LONG_CONTEXT
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
+    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((B, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=wl.chunk)
+    nws = P.scan_workspace_bytes(desc)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"],
+                                inp["z"], inp["Dskip"], None, y, hT, ws, nws)
+    run()
+    l_ms = time_events(run, 5)
+    nb = scan_bytes(B, L, D, N)
+    res["long_context"] = {"workload": wl.name, "ms": l_ms, "tokens_per_s": B * L / (l_ms * 1e-3),
+                           "gbps": nb / (l_ms * 1e-3) / 1e9}
+    del inp, y, hT, ws
+    torch.cuda.empty_cache()
+
+    # one layer of the large corpus encode (state-only)
+    wl = synth.LARGE_CORPUS
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, wl.dt_mu, wl.dt_sigma,
+                                   need_z_c=False)
+    store = torch.empty((B, 24, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.F32, P.F16, hT_batch_stride=24 * D * N)
+    run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
+                                None, None, None, store[:, 0])
+    run()
+    c_ms = time_events(run, 3)
+    nb = scan_bytes(B, L, D, N, readout=False)
+    res["large_corpus_layer"] = {"workload": wl.name, "ms": c_ms,
+                                 "tokens_per_s": B * L / (c_ms * 1e-3),
+                                 "gbps": nb / (c_ms * 1e-3) / 1e9,
+                                 "exp_per_s": B * L * D * N / (c_ms * 1e-3)}
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--extra", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the scan, retrieval and injection "
+              "kernels run on a single MI355X and no multi-GPU path is built; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    out = bench_corpus(args)
+    if args.extra:
+        out["extra"] = bench_extra(args)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,167 @@
+/*
+ * precog.h -- C ABI of libprecog: the PRECOG hot path on one MI355X (gfx950).
+ *
+ * PRECOG (arXiv 2608.02560) encodes each corpus chunk once into the final
+ * recurrent state of a gated selective SSM, stores that state, and at query
+ * time retrieves the best-matching state by cosine similarity, injects it as
+ * the initial state and runs only the query tokens (Sec. 4.2).  Theorem 1
+ * (Sec. 4.3) makes the injection exact: S(h0, c ++ q) = S(S(h0, c), q).
+ *
+ * The three operations of that path are exported here:
+ *   precog_scan_encode      selective-SSM prefill scan with injectable h0 and
+ *                           captured hT (Eq. 1, Sec. 3; capture, Sec. 4.2)
+ *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
+ *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are device pointers owned by the caller.  The
+ *     library never allocates, frees, copies between host and device, or
+ *     synchronises; work is enqueued on `stream` (a hipStream_t passed as
+ *     void*, NULL = the default stream) and runs asynchronously.
+ *   - Arguments are validated on the host before anything is enqueued.  On a
+ *     validation failure nothing is written and the status says why.  A HIP
+ *     launch failure returns PRECOG_ERR_HIP.  No C++ exception crosses the
+ *     ABI.  The only library state is a per-device cache of the architecture
+ *     check.
+ *   - Layouts are row-major with the last index fastest.
+ *   - Entry points may be called concurrently from several host threads on
+ *     different streams; calls on one stream execute in order.
+ */
+#ifndef PRECOG_H
+#define PRECOG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PRECOG_F32 = 0,  /* IEEE binary32 */
+    PRECOG_BF16 = 1, /* bfloat16 (upper half of binary32) */
+    PRECOG_F16 = 2   /* IEEE binary16 */
+} precog_dtype;
+
+typedef enum {
+    PRECOG_OK = 0,
+    PRECOG_ERR_NULL = 1,      /* a required pointer is NULL */
+    PRECOG_ERR_SHAPE = 2,     /* negative size, unsupported N, E, ... */
+    PRECOG_ERR_DTYPE = 3,     /* dtype not supported for that tensor */
+    PRECOG_ERR_STRIDE = 4,    /* state batch stride smaller than D*N */
+    PRECOG_ERR_ALIGN = 5,     /* pointer or size breaks the alignment rule */
+    PRECOG_ERR_WORKSPACE = 6, /* workspace missing or too small */
+    PRECOG_ERR_ARCH = 7,      /* current device is not gfx950 */
+    PRECOG_ERR_HIP = 8        /* a HIP runtime call or launch failed */
+} precog_status;
+
+/* ------------------------------------------------------------------------ */
+/* Selective-SSM prefill scan                                               */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t batch;  /* B: independent sequences (corpus chunks or queries) */
+    int64_t seqlen; /* L: tokens per sequence, >= 0 */
+    int64_t dim;    /* D: channels, a multiple of 8 */
+    int64_t dstate; /* N: state size per channel, one of 1,2,4,8,16,32,64 */
+    precog_dtype in_dtype;    /* x, dt, B, C, z: PRECOG_F32 or PRECOG_BF16 */
+    precog_dtype out_dtype;   /* y: PRECOG_F32 or PRECOG_BF16 */
+    precog_dtype state_dtype; /* h0 and hT storage: PRECOG_F32 or PRECOG_F16;
+                                 the running state is always fp32 */
+    int64_t h0_batch_stride;  /* elements between batch rows of h0; 0 = D*N */
+    int64_t hT_batch_stride;  /* elements between batch rows of hT; 0 = D*N
+                                 (e.g. layers*D*N to land each final state
+                                 in its layer slot of a [chunks, layers, D, N]
+                                 store) */
+    int64_t chunk;            /* time-chunk length of the two-level scan:
+                                 0 = chosen by the library; >= L = one pass */
+} precog_scan_desc;
+
+/* Bytes of device workspace precog_scan_encode needs for `desc` (0 when the
+ * scan runs in one pass).  Returns 0 for an invalid descriptor too; the
+ * encode call reports the error. */
+size_t precog_scan_workspace_bytes(const precog_scan_desc *desc);
+
+/* The recurrence of Eq. 1 (Sec. 3) with a real, positive diagonal A, rolled
+ * over each sequence from h0 (the rollout S(h0, x_1:L) of App. A):
+ *
+ *   h_t[d,n] = exp(-dt_t[d] * A[d,n]) * h_{t-1}[d,n] + B_t[n] * x_t[d] * dt_t[d]
+ *   y_t[d]   = (sum_n C_t[n] h_t[d,n] + Dskip[d] x_t[d]) * silu(z_t[d])
+ *   hT       = h_L   (the state after the last token; offline indexing
+ *                     captures it, Sec. 4.2)
+ *
+ * with silu(v) = v / (1 + exp(-v)) and t = 1..L per batch row.  Arguments:
+ *   x, dt, z   [B, L, D] in desc->in_dtype.  dt > 0 (already a timescale;
+ *              no softplus is applied).  z NULL = no gate (factor 1).
+ *   A          [D, N] fp32, A > 0 (decay < 1: the stable SSM of App. A).
+ *   B, C       [B, L, N] in desc->in_dtype, shared by all channels.
+ *   Dskip      [D] fp32; NULL = no skip term.
+ *   h0         state rows in desc->state_dtype, row b at h0 + b*stride, each
+ *              row [D, N]; NULL = zero initial state.
+ *   y          [B, L, D] in desc->out_dtype; NULL = state-only encode (then C,
+ *              z and Dskip are not read and may be NULL).
+ *   hT         state rows like h0 (its own stride); NULL = not captured.
+ *              hT may alias h0 exactly (in-place streaming prefill: the
+ *              state of one call becomes the injected state of the next).
+ *   workspace  device memory of precog_scan_workspace_bytes(desc) bytes,
+ *              16-byte aligned (NULL allowed when that size is 0).
+ * Alignment: every tensor base pointer 16-byte aligned, D % 8 == 0, state
+ * strides % 8 == 0.  y must not overlap any input.  Results are
+ * deterministic: the same inputs give bitwise the same outputs. */
+precog_status precog_scan_encode(const precog_scan_desc *desc, const void *x,
+                                 const void *dt, const float *A, const void *B,
+                                 const void *C, const void *z,
+                                 const float *Dskip, const void *h0, void *y,
+                                 void *hT, void *workspace,
+                                 size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Cosine top-1 retrieval                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace precog_retrieve_top1 needs for (Q, M, E). */
+size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E);
+
+/* Query-time retrieval of Sec. 4.2: for each query q,
+ *   idx[q] = argmax_i <query[q], index[i]>
+ * over the M key rows, the cosine similarity for unit-norm rows.  The result
+ * is exact: it equals the argmax of the fp64 inner products summed in index
+ * order (products of fp32 values are exact in fp64), ties going to the
+ * lowest row.  An fp32 matrix-core screen proposes candidates within a
+ * proven error margin and only those are rescored in fp64.
+ *   query_emb  [Q, E] fp32     index_emb [M, E] fp32 (rows of any norm;
+ *              the margin scales with the row norms)
+ *   idx        [Q] int32 output; M == 0 gives -1
+ *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
+ *   workspace  precog_retrieve_workspace_bytes(Q, M, E) bytes, 16-byte
+ *              aligned. */
+precog_status precog_retrieve_top1(const float *query_emb,
+                                   const float *index_emb, int64_t Q, int64_t M,
+                                   int64_t E, int32_t *idx, void *workspace,
+                                   size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* State injection                                                          */
+/* ------------------------------------------------------------------------ */
+
+/* The injection of Sec. 4.2, h_init <- h^(i*): copies state rows of S
+ * elements (e.g. D*N for one layer, layers*D*N for a whole model state)
+ *   h0[q, :] = store[idx[q], :]     for q = 0..Q-1
+ * from store [M, S] (store_dtype F32 or F16) into h0 [Q, S] (h0_dtype F32 or
+ * F16; F16 -> F32 widens exactly, F32 -> F16 rounds to nearest even).
+ * An idx outside [0, M) fills that row of h0 with NaN and reads nothing.
+ * S % 8 == 0; pointers 16-byte aligned. */
+precog_status precog_inject_gather(const void *state_store,
+                                   precog_dtype store_dtype, int64_t M,
+                                   int64_t S, const int32_t *idx, int64_t Q,
+                                   void *h0, precog_dtype h0_dtype,
+                                   void *stream);
+
+/* Static, human-readable name of a status code. */
+const char *precog_status_string(precog_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRECOG_H */

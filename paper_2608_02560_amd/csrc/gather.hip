@@ -1,0 +1,88 @@
+// State injection for gfx950 (query time, Sec. 4.2): h0[q] = store[idx[q]].
+//
+// Pure data movement: each lane moves 8 consecutive elements (16 bytes of
+// fp16 or 32 bytes of fp32) so every wave access is a contiguous 1-2 KiB
+// segment.  fp16 -> fp32 widening is exact; fp32 -> fp16 rounds to nearest
+// even.  An index outside [0, M) reads nothing and writes NaN.
+#include "precog_kernels.h"
+
+namespace precog {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kVec = 8;
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float8 __attribute__((ext_vector_type(8)));
+
+template <typename T> struct Vec8;
+template <> struct Vec8<float> {
+  static __device__ __forceinline__ float8 load(const void* base, int64_t i) {
+    return *reinterpret_cast<const float8*>(static_cast<const float*>(base) + i);
+  }
+  static __device__ __forceinline__ void store(void* base, int64_t i, float8 v) {
+    *reinterpret_cast<float8*>(static_cast<float*>(base) + i) = v;
+  }
+};
+template <> struct Vec8<f16_t> {
+  static __device__ __forceinline__ float8 load(const void* base, int64_t i) {
+    const half8 h = *reinterpret_cast<const half8*>(static_cast<const _Float16*>(base) + i);
+    return __builtin_convertvector(h, float8);
+  }
+  static __device__ __forceinline__ void store(void* base, int64_t i, float8 v) {
+    *reinterpret_cast<half8*>(static_cast<_Float16*>(base) + i) = __builtin_convertvector(v, half8);
+  }
+};
+
+template <typename TS, typename TO>
+__global__ __launch_bounds__(kBlock) void gather_kernel(const GatherParams p) {
+  const int64_t q = blockIdx.y;
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kVec;
+  if (e >= p.S) return;
+  const int32_t src = p.idx[q];
+  float8 v;
+  if (src >= 0 && src < p.M) {
+    v = Vec8<TS>::load(p.store, static_cast<int64_t>(src) * p.S + e);
+  } else {
+    const float nan = __builtin_nanf("");
+    v = float8{nan, nan, nan, nan, nan, nan, nan, nan};
+  }
+  Vec8<TO>::store(p.out, q * p.S + e, v);
+}
+
+// Same-dtype copy: move raw 16-byte words, no conversion.
+__global__ __launch_bounds__(kBlock) void gather_raw_kernel(const GatherParams p, int64_t words_per_row,
+                                                            int elem_bytes) {
+  const int64_t q = blockIdx.y;
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (w >= words_per_row) return;
+  const int32_t src = p.idx[q];
+  uint4 v;
+  if (src >= 0 && src < p.M) {
+    v = reinterpret_cast<const uint4*>(p.store)[static_cast<int64_t>(src) * words_per_row + w];
+  } else {
+    const uint32_t nan = elem_bytes == 4 ? 0x7fc00000u : 0x7e007e00u;
+    v = make_uint4(nan, nan, nan, nan);
+  }
+  reinterpret_cast<uint4*>(p.out)[q * words_per_row + w] = v;
+}
+
+}  // namespace
+
+hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype, hipStream_t s) {
+  if (store_dtype == out_dtype) {
+    const int eb = store_dtype == 0 ? 4 : 2;
+    const int64_t words = p.S * eb / 16;
+    const dim3 grid(static_cast<unsigned>((words + kBlock - 1) / kBlock), static_cast<unsigned>(p.Q));
+    hipLaunchKernelGGL(gather_raw_kernel, grid, dim3(kBlock), 0, s, p, words, eb);
+  } else {
+    const dim3 grid(static_cast<unsigned>((p.S / kVec + kBlock - 1) / kBlock), static_cast<unsigned>(p.Q));
+    if (store_dtype == 2)
+      hipLaunchKernelGGL((gather_kernel<f16_t, float>), grid, dim3(kBlock), 0, s, p);
+    else
+      hipLaunchKernelGGL((gather_kernel<float, f16_t>), grid, dim3(kBlock), 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace precog

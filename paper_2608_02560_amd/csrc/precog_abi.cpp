@@ -1,0 +1,275 @@
+// C-ABI layer of libprecog: host-side validation, chunk selection and
+// launches.  Declared in include/precog.h.  Nothing here allocates, copies
+// between host and device or synchronises.
+#include "precog.h"
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstring>
+
+#include "precog_kernels.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+// 0 = unknown, 1 = gfx950, 2 = other architecture
+std::atomic<int> g_arch_ok[kMaxDevices];
+
+precog_status check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return PRECOG_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return PRECOG_ERR_ARCH;
+  int st = g_arch_ok[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return PRECOG_ERR_HIP;
+    st = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_arch_ok[dev].store(st, std::memory_order_relaxed);
+  }
+  return st == 1 ? PRECOG_OK : PRECOG_ERR_ARCH;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_n(int64_t n) {
+  return n == 1 || n == 2 || n == 4 || n == 8 || n == 16 || n == 32 || n == 64;
+}
+
+constexpr int64_t kBlock = 256;           // channels per scan workgroup
+constexpr int64_t kTargetWaves = 2048;    // 2 waves per SIMD on 256 CUs
+constexpr int64_t kMinAutoChunk = 64;
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int64_t auto_chunk(const precog_scan_desc* d);
+
+// Longest chunk whose per-token streams stay addressable with the kernels'
+// 32-bit buffer offsets: chunk * D * 4 bytes (the widest element) < 2^31.
+int64_t max_chunk(const precog_scan_desc* d) {
+  const int64_t row = (d->dim > 0 ? d->dim : 1) * 4;
+  return ((1LL << 31) - 1) / row;
+}
+
+// Time-chunk length used for a descriptor (after validation).
+int64_t effective_chunk(const precog_scan_desc* d) {
+  const int64_t L = d->seqlen;
+  if (L <= 0) return 1;
+  const int64_t cap = max_chunk(d);
+  if (d->chunk > 0) {
+    const int64_t c = d->chunk >= L ? L : d->chunk;
+    return c < cap ? c : cap;
+  }
+  if (L <= cap) return auto_chunk(d);
+  const int64_t a = auto_chunk(d);
+  return a < cap ? a : cap;
+}
+
+// Auto policy: one pass when batch x channel waves already fill the SIMDs;
+// otherwise cut time so that about kTargetWaves waves run.
+int64_t auto_chunk(const precog_scan_desc* d) {
+  const int64_t L = d->seqlen;
+  const int64_t waves = d->batch * ceil_div(d->dim, 64);
+  if (waves >= kTargetWaves || L <= 2 * kMinAutoChunk) return L;
+  int64_t nch = ceil_div(kTargetWaves, waves > 0 ? waves : 1);
+  const int64_t max_nch = L / kMinAutoChunk;
+  if (nch > max_nch) nch = max_nch;
+  if (nch <= 1) return L;
+  return ceil_div(L, nch);
+}
+
+size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+struct ScanWs {
+  size_t carry_bytes, dtsum_bytes, total;
+};
+
+ScanWs scan_ws(const precog_scan_desc* d, int64_t nchunks) {
+  ScanWs w{0, 0, 0};
+  if (nchunks <= 1) return w;
+  w.carry_bytes = align_up(static_cast<size_t>(d->batch) * nchunks * d->dim * d->dstate * 4);
+  w.dtsum_bytes = align_up(static_cast<size_t>(d->batch) * nchunks * d->dim * 4);
+  w.total = w.carry_bytes + w.dtsum_bytes;
+  return w;
+}
+
+precog_status validate_desc(const precog_scan_desc* d) {
+  if (!d) return PRECOG_ERR_NULL;
+  if (d->batch < 0 || d->seqlen < 0 || d->dim < 0 || d->chunk < 0) return PRECOG_ERR_SHAPE;
+  if (!valid_n(d->dstate)) return PRECOG_ERR_SHAPE;
+  if (d->batch > (1LL << 30) || d->dim > (1LL << 24) || d->seqlen > (1LL << 40))
+    return PRECOG_ERR_SHAPE;
+  if (d->in_dtype != PRECOG_F32 && d->in_dtype != PRECOG_BF16) return PRECOG_ERR_DTYPE;
+  if (d->out_dtype != PRECOG_F32 && d->out_dtype != PRECOG_BF16) return PRECOG_ERR_DTYPE;
+  if (d->state_dtype != PRECOG_F32 && d->state_dtype != PRECOG_F16) return PRECOG_ERR_DTYPE;
+  const int64_t dn = d->dim * d->dstate;
+  if (d->h0_batch_stride != 0 && d->h0_batch_stride < dn) return PRECOG_ERR_STRIDE;
+  if (d->hT_batch_stride != 0 && d->hT_batch_stride < dn) return PRECOG_ERR_STRIDE;
+  if (d->dim % 8 != 0) return PRECOG_ERR_ALIGN;
+  if (d->h0_batch_stride % 8 != 0 || d->hT_batch_stride % 8 != 0) return PRECOG_ERR_ALIGN;
+  return PRECOG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* precog_status_string(precog_status s) {
+  switch (s) {
+    case PRECOG_OK: return "ok";
+    case PRECOG_ERR_NULL: return "a required pointer is NULL";
+    case PRECOG_ERR_SHAPE: return "unsupported or negative size";
+    case PRECOG_ERR_DTYPE: return "unsupported dtype for this tensor";
+    case PRECOG_ERR_STRIDE: return "state batch stride smaller than D*N";
+    case PRECOG_ERR_ALIGN: return "pointer or size breaks the alignment rule";
+    case PRECOG_ERR_WORKSPACE: return "workspace missing or too small";
+    case PRECOG_ERR_ARCH: return "current device is not gfx950";
+    case PRECOG_ERR_HIP: return "HIP runtime call or launch failed";
+  }
+  return "unknown status";
+}
+
+size_t precog_scan_workspace_bytes(const precog_scan_desc* desc) {
+  if (validate_desc(desc) != PRECOG_OK) return 0;
+  const int64_t ch = effective_chunk(desc);
+  const int64_t nch = desc->seqlen > 0 ? ceil_div(desc->seqlen, ch) : 1;
+  return scan_ws(desc, nch).total;
+}
+
+precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, const void* dt,
+                                 const float* A, const void* B, const void* C, const void* z,
+                                 const float* Dskip, const void* h0, void* y, void* hT,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  precog_status st = validate_desc(desc);
+  if (st != PRECOG_OK) return st;
+  const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
+  if (Bt == 0 || D == 0) return PRECOG_OK;  // nothing to compute
+  const bool work = L > 0;
+  if (!A) return PRECOG_ERR_NULL;
+  if (work && (!x || !dt || !B)) return PRECOG_ERR_NULL;
+  if (work && y && !C) return PRECOG_ERR_NULL;
+  if (!y && !hT) return PRECOG_OK;  // nothing requested
+  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, y, hT, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+
+  const int64_t chunk = effective_chunk(desc);
+  const int64_t nchunks = work ? ceil_div(L, chunk) : 1;
+  if (nchunks > (1LL << 20)) return PRECOG_ERR_SHAPE;
+  const ScanWs ws = scan_ws(desc, nchunks);
+  if (ws.total > 0 && (!workspace || workspace_bytes < ws.total)) return PRECOG_ERR_WORKSPACE;
+  const int64_t dblocks = ceil_div(D, kBlock);
+  if (dblocks * Bt * nchunks > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (Bt * D * N / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+
+  st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  precog::ScanParams p{};
+  p.x = x;
+  p.dt = dt;
+  p.z = y ? z : nullptr;
+  p.Bm = B;
+  p.Cm = y ? C : nullptr;
+  p.A = A;
+  p.Dskip = y ? Dskip : nullptr;
+  p.h0 = h0;
+  p.y = work ? y : nullptr;
+  p.hT = hT;
+  p.carry = ws.total ? static_cast<float*>(workspace) : nullptr;
+  p.dtsum = ws.total ? reinterpret_cast<float*>(static_cast<char*>(workspace) + ws.carry_bytes)
+                     : nullptr;
+  p.B = Bt;
+  p.L = L;
+  p.D = D;
+  p.chunk = chunk;
+  p.h0_stride = desc->h0_batch_stride ? desc->h0_batch_stride : D * N;
+  p.hT_stride = desc->hT_batch_stride ? desc->hT_batch_stride : D * N;
+  p.nchunks = static_cast<int>(nchunks);
+  p.dblocks = static_cast<int>(dblocks);
+  p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
+            (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
+  if (!p.y && !p.hT) return PRECOG_OK;  // L == 0 and no state requested
+
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_scan(p, static_cast<int>(N), desc->in_dtype,
+                                           desc->out_dtype, desc->state_dtype,
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
+size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E) {
+  if (Q < 0 || M < 0 || E < 4 || E > 4096 || E % 4 != 0) return 0;
+  return align_up(static_cast<size_t>(Q) * M * 4) + align_up(static_cast<size_t>(M) * 4);
+}
+
+precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
+                                   int64_t M, int64_t E, int32_t* idx, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
+  if (E % 4 != 0) return PRECOG_ERR_ALIGN;
+  if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (Q == 0) return PRECOG_OK;
+  if (!query_emb || !idx) return PRECOG_ERR_NULL;
+  if (M > 0 && !index_emb) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {query_emb, index_emb, idx, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  const size_t need = precog_retrieve_workspace_bytes(Q, M, E);
+  if (M > 0 && (!workspace || workspace_bytes < need)) return PRECOG_ERR_WORKSPACE;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  precog::RetrieveParams p{};
+  p.q = query_emb;
+  p.K = index_emb;
+  p.scores = M > 0 ? static_cast<float*>(workspace) : nullptr;
+  p.rownorm2 = M > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                                align_up(static_cast<size_t>(Q) * M * 4))
+                     : nullptr;
+  p.idx = idx;
+  p.Q = Q;
+  p.M = M;
+  p.E = E;
+  p.ld_scores = M;
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_retrieve(p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
+precog_status precog_inject_gather(const void* state_store, precog_dtype store_dtype, int64_t M,
+                                   int64_t S, const int32_t* idx, int64_t Q, void* h0,
+                                   precog_dtype h0_dtype, void* stream) {
+  if (M < 0 || S < 0 || Q < 0) return PRECOG_ERR_SHAPE;
+  if ((store_dtype != PRECOG_F32 && store_dtype != PRECOG_F16) ||
+      (h0_dtype != PRECOG_F32 && h0_dtype != PRECOG_F16))
+    return PRECOG_ERR_DTYPE;
+  if (S % 8 != 0) return PRECOG_ERR_ALIGN;
+  if (Q == 0 || S == 0) return PRECOG_OK;
+  if (!idx || !h0 || (M > 0 && !state_store)) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {state_store, idx, h0};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  if (S / 8 / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  (void)hipGetLastError();
+  const int out_bytes = h0_dtype == PRECOG_F32 ? 4 : 2;
+  // gridDim.y is limited to 65535: walk the queries in slices.
+  for (int64_t q0 = 0; q0 < Q; q0 += 65535) {
+    precog::GatherParams p{};
+    p.store = state_store;
+    p.idx = idx + q0;
+    p.out = static_cast<char*>(h0) + q0 * S * out_bytes;
+    p.M = M;
+    p.S = S;
+    p.Q = (Q - q0) < 65535 ? (Q - q0) : 65535;
+    const hipError_t e = precog::launch_gather(p, store_dtype, h0_dtype,
+                                               static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return PRECOG_ERR_HIP;
+  }
+  return PRECOG_OK;
+}
+
+}  // extern "C"

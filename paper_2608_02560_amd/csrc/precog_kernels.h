@@ -1,0 +1,81 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer of
+// libprecog (not part of the public interface, which is include/precog.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace precog {
+
+// Storage tags.  bf16 and fp16 are both 16-bit; the tags keep them apart.
+struct bf16_t { uint16_t bits; };
+struct f16_t { uint16_t bits; };
+
+enum ScanFlags : int {
+  kHasZ = 1,   // gate z present
+  kHasD = 2,   // Dskip present
+  kHasH0 = 4,  // initial state present
+  kHasHT = 8,  // final state requested
+};
+
+// Everything one scan launch needs.  Passed by value as the kernel argument.
+struct ScanParams {
+  const void* x;
+  const void* dt;
+  const void* z;
+  const void* Bm;
+  const void* Cm;
+  const float* A;
+  const float* Dskip;
+  const void* h0;
+  void* y;
+  void* hT;
+  float* carry;   // [B, C, D, N] fp32: slot 0 = h0, slot c = state entering chunk c
+  float* dtsum;   // [B, C, D] fp32: slot c = sum of dt over chunk c (c < C-1)
+  int64_t B, L, D;
+  int64_t chunk;  // tokens per time chunk
+  int64_t h0_stride, hT_stride;
+  int nchunks;    // C
+  int dblocks;    // ceil(D / 256)
+  int flags;
+};
+
+// Launchers (return the HIP launch status).  in/out/state dtypes are the
+// precog_dtype codes of the public header.
+hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
+                       int state_dtype, hipStream_t s);
+
+struct RetrieveParams {
+  const float* q;      // [Q, E]
+  const float* K;      // [M, E]
+  float* scores;       // [Q, M] fp32 screen scores (workspace)
+  float* rownorm2;     // [M] fp32 squared row norms (workspace)
+  int32_t* idx;        // [Q]
+  int64_t Q, M, E;
+  int64_t ld_scores;   // row pitch of `scores` in elements
+};
+hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
+
+struct GatherParams {
+  const void* store;  // [M, S]
+  const int32_t* idx; // [Q]
+  void* out;          // [Q, S]
+  int64_t M, S, Q;
+};
+hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype,
+                         hipStream_t s);
+
+// Maps a hardware workgroup id to a logical one so that logically adjacent
+// workgroups run on the same XCD (the dispatcher deals workgroups to the 8
+// XCDs round-robin, and each XCD has its own L2).
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  const int kXcd = 8;
+  const int xcd = bid % kXcd;
+  const int local = bid / kXcd;
+  const int per = nblocks / kXcd;
+  const int rem = nblocks % kXcd;
+  return xcd < rem ? xcd * (per + 1) + local
+                   : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+}  // namespace precog

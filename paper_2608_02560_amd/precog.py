@@ -1,0 +1,177 @@
+"""Python binding of libprecog (the C ABI in include/precog.h).
+
+Argument marshalling only: every step of the computation runs in the gfx950
+kernels of libprecog.so.  PyTorch supplies device memory and the current
+HIP stream.  There is no fallback: if the library is missing or the device is
+not a gfx950, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libprecog.so")
+
+F32, BF16, F16 = 0, 1, 2
+_DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+
+STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECOG_ERR_DTYPE",
+          4: "PRECOG_ERR_STRIDE", 5: "PRECOG_ERR_ALIGN", 6: "PRECOG_ERR_WORKSPACE",
+          7: "PRECOG_ERR_ARCH", 8: "PRECOG_ERR_HIP"}
+
+EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode",
+           "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
+           "precog_inject_gather", "precog_status_string")
+
+
+class PrecogError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (fn, STATUS.get(status, status),
+                                                 status_string(status)))
+
+
+class ScanDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+                ("dim", ctypes.c_int64), ("dstate", ctypes.c_int64),
+                ("in_dtype", ctypes.c_int), ("out_dtype", ctypes.c_int),
+                ("state_dtype", ctypes.c_int),
+                ("h0_batch_stride", ctypes.c_int64), ("hT_batch_stride", ctypes.c_int64),
+                ("chunk", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libprecog.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libprecog.so is not built (%s); run "
+                               "`python -m paper_2608_02560_amd.build`" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+        L.precog_scan_workspace_bytes.argtypes = [ctypes.POINTER(ScanDesc)]
+        L.precog_scan_workspace_bytes.restype = sz
+        L.precog_scan_encode.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + [sz, vp]
+        L.precog_scan_encode.restype = ctypes.c_int
+        L.precog_retrieve_workspace_bytes.argtypes = [i64, i64, i64]
+        L.precog_retrieve_workspace_bytes.restype = sz
+        L.precog_retrieve_top1.argtypes = [vp, vp, i64, i64, i64, vp, vp, sz, vp]
+        L.precog_retrieve_top1.restype = ctypes.c_int
+        L.precog_inject_gather.argtypes = [vp, ctypes.c_int, i64, i64, vp, i64, vp,
+                                           ctypes.c_int, vp]
+        L.precog_inject_gather.restype = ctypes.c_int
+        L.precog_status_string.argtypes = [ctypes.c_int]
+        L.precog_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().precog_status_string(int(status)).decode()
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(fn, st):
+    if st != 0:
+        raise PrecogError(fn, st)
+
+
+def scan_desc(batch, seqlen, dim, dstate, in_dtype=BF16, out_dtype=F32, state_dtype=F32,
+              h0_batch_stride=0, hT_batch_stride=0, chunk=0) -> ScanDesc:
+    return ScanDesc(batch, seqlen, dim, dstate, in_dtype, out_dtype, state_dtype,
+                    h0_batch_stride, hT_batch_stride, chunk)
+
+
+def scan_workspace_bytes(desc: ScanDesc) -> int:
+    return int(lib().precog_scan_workspace_bytes(ctypes.byref(desc)))
+
+
+def scan_encode(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None, y=None,
+                hT=None, workspace=None, workspace_bytes=0, stream=None):
+    """precog_scan_encode on device tensors (or raw device pointers)."""
+    st = lib().precog_scan_encode(ctypes.byref(desc), _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
+                                  _ptr(C), _ptr(z), _ptr(Dskip), _ptr(h0), _ptr(y), _ptr(hT),
+                                  _ptr(workspace), int(workspace_bytes), _stream(stream))
+    _check("precog_scan_encode", st)
+
+
+def retrieve_workspace_bytes(Q, M, E) -> int:
+    return int(lib().precog_retrieve_workspace_bytes(Q, M, E))
+
+
+def retrieve_top1(query, index, idx, workspace, workspace_bytes=None, stream=None):
+    Q, E = query.shape
+    M = index.shape[0]
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib().precog_retrieve_top1(_ptr(query), _ptr(index), Q, M, E, _ptr(idx),
+                                    _ptr(workspace), int(workspace_bytes), _stream(stream))
+    _check("precog_retrieve_top1", st)
+
+
+def inject_gather(store, idx, h0, stream=None):
+    M = store.shape[0]
+    S = store[0].numel() if M > 0 else h0[0].numel()
+    st = lib().precog_inject_gather(_ptr(store), _DT[store.dtype], M, S, _ptr(idx),
+                                    idx.shape[0], _ptr(h0), _DT[h0.dtype], _stream(stream))
+    _check("precog_inject_gather", st)
+
+
+# ----------------------------------------------------------------------------
+# Convenience wrappers that allocate outputs and workspace with torch.
+# ----------------------------------------------------------------------------
+def scan(x, dt, A, B, C=None, z=None, Dskip=None, h0=None, *, out_dtype=torch.float32,
+         state_dtype=torch.float32, want_y=True, want_hT=True, chunk=0, hT=None,
+         hT_batch_stride=0, h0_batch_stride=0, stream=None):
+    """Runs the scan; returns (y, hT) (None where not requested)."""
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[state_dtype],
+                     h0_batch_stride, hT_batch_stride, chunk)
+    y = torch.empty((Bt, L, D), dtype=out_dtype, device=x.device) if want_y else None
+    if want_hT and hT is None:
+        hT = torch.empty((Bt, D, N), dtype=state_dtype, device=x.device)
+    nbytes = scan_workspace_bytes(desc)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    scan_encode(desc, x, dt, A, B, C, z, Dskip, h0, y, hT if want_hT else None, ws, nbytes,
+                stream)
+    return y, (hT if want_hT else None)
+
+
+def top1(query, index, stream=None):
+    Q, E = query.shape
+    M = index.shape[0]
+    idx = torch.empty(Q, dtype=torch.int32, device=query.device)
+    nbytes = retrieve_workspace_bytes(Q, M, E)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=query.device)
+    retrieve_top1(query, index, idx, ws, nbytes, stream)
+    return idx
+
+
+def gather(store, idx, out_dtype=None, stream=None):
+    out_dtype = out_dtype or store.dtype
+    h0 = torch.empty((idx.shape[0],) + tuple(store.shape[1:]), dtype=out_dtype,
+                     device=store.device)
+    inject_gather(store, idx, h0, stream)
+    return h0

@@ -1,0 +1,137 @@
+"""Host-only checks of libprecog: it loads, exports every entry point the
+public header declares, and rejects malformed arguments with the documented
+status before anything touches a GPU (no compute calls are made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_02560_amd import precog as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "precog.h")
+
+OK, ENULL, ESHAPE, EDTYPE, ESTRIDE, EALIGN, EWS = 0, 1, 2, 3, 4, 5, 6
+
+FAKE = 0x10000  # a 16-byte aligned non-null address; never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(precog_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = P.lib()
+    names = declared_functions()
+    assert set(names) == set(P.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for code in range(9):
+        assert P.status_string(code)
+    assert P.status_string(99) == "unknown status"
+
+
+def _encode(desc, x=FAKE, dt=FAKE, A=FAKE, B=FAKE, C=FAKE, z=FAKE, Dskip=FAKE, h0=None,
+            y=FAKE, hT=FAKE, ws=None, wsb=0):
+    d = desc if desc is None else ctypes.byref(desc)
+    return P.lib().precog_scan_encode(d, x, dt, A, B, C, z, Dskip, h0, y, hT, ws, wsb, None)
+
+
+def test_scan_validation_errors():
+    good = P.scan_desc(2, 16, 64, 16)
+    assert _encode(None) == ENULL
+    assert _encode(P.scan_desc(-1, 16, 64, 16)) == ESHAPE
+    assert _encode(P.scan_desc(2, -1, 64, 16)) == ESHAPE
+    assert _encode(P.scan_desc(2, 16, 64, 3)) == ESHAPE        # N not supported
+    assert _encode(P.scan_desc(2, 16, 64, 128)) == ESHAPE
+    assert _encode(P.scan_desc(2, 16, 60, 16)) == EALIGN       # D % 8
+    assert _encode(P.scan_desc(2, 16, 64, 16, in_dtype=P.F16)) == EDTYPE
+    assert _encode(P.scan_desc(2, 16, 64, 16, out_dtype=P.F16)) == EDTYPE
+    assert _encode(P.scan_desc(2, 16, 64, 16, state_dtype=P.BF16)) == EDTYPE
+    assert _encode(P.scan_desc(2, 16, 64, 16, h0_batch_stride=64 * 16 - 8)) == ESTRIDE
+    assert _encode(P.scan_desc(2, 16, 64, 16, hT_batch_stride=4)) == ESTRIDE
+    assert _encode(P.scan_desc(2, 16, 64, 16, hT_batch_stride=64 * 16 + 4)) == EALIGN
+    assert _encode(good, x=None) == ENULL
+    assert _encode(good, dt=None) == ENULL
+    assert _encode(good, A=None) == ENULL
+    assert _encode(good, B=None) == ENULL
+    assert _encode(good, C=None) == ENULL                       # C needed for y
+    assert _encode(good, x=FAKE + 2) == EALIGN
+    assert _encode(good, hT=FAKE + 8) == EALIGN
+    # chunked scans need workspace
+    chunked = P.scan_desc(2, 1024, 64, 16, chunk=128)
+    need = P.scan_workspace_bytes(chunked)
+    assert need > 0
+    assert _encode(chunked) == EWS
+    assert _encode(chunked, ws=FAKE, wsb=need - 1) == EWS
+
+
+def test_scan_noops_return_ok_without_device():
+    # nothing to compute: empty batch, empty channels, or no output requested
+    assert _encode(P.scan_desc(0, 16, 64, 16)) == OK
+    assert _encode(P.scan_desc(2, 16, 0, 16)) == OK
+    assert _encode(P.scan_desc(2, 16, 64, 16), y=None, hT=None) == OK
+    # y = NULL makes C, z and Dskip optional
+    st = _encode(P.scan_desc(0, 16, 64, 16), C=None, z=None, Dskip=None, y=None)
+    assert st == OK
+
+
+def test_scan_workspace_sizes():
+    assert P.scan_workspace_bytes(P.scan_desc(64, 3000, 2048, 16)) == 0  # one pass
+    d = P.scan_desc(8, 65536, 2048, 16, chunk=256)
+    C = 256
+    carry = 8 * C * 2048 * 16 * 4
+    dts = 8 * C * 2048 * 4
+    assert P.scan_workspace_bytes(d) == carry + dts
+    # chunk >= L is one pass
+    assert P.scan_workspace_bytes(P.scan_desc(2, 100, 64, 16, chunk=100)) == 0
+    assert P.scan_workspace_bytes(P.scan_desc(2, 100, 64, 16, chunk=1000)) == 0
+    # invalid descriptor reports 0
+    assert P.scan_workspace_bytes(P.scan_desc(2, 100, 60, 16)) == 0
+
+
+def test_retrieve_validation_errors():
+    L = P.lib()
+    ws = P.retrieve_workspace_bytes(4, 10, 16)
+    assert ws >= 4 * 10 * 4 + 10 * 4
+    call = lambda q=FAKE, k=FAKE, Q=4, M=10, E=16, idx=FAKE, w=FAKE, wb=ws: \
+        L.precog_retrieve_top1(q, k, Q, M, E, idx, w, wb, None)
+    assert call(Q=-1) == ESHAPE
+    assert call(E=2) == ESHAPE
+    assert call(E=8192) == ESHAPE
+    assert call(E=18) == EALIGN
+    assert call(q=None) == ENULL
+    assert call(k=None) == ENULL
+    assert call(idx=None) == ENULL
+    assert call(w=None) == EWS
+    assert call(wb=ws - 1) == EWS
+    assert call(q=FAKE + 4) == EALIGN
+    assert call(Q=0) == OK
+
+
+def test_gather_validation_errors():
+    L = P.lib()
+    call = lambda s=FAKE, sd=P.F16, M=10, S=64, idx=FAKE, Q=3, h=FAKE, hd=P.F32: \
+        L.precog_inject_gather(s, sd, M, S, idx, Q, h, hd, None)
+    assert call(M=-1) == ESHAPE
+    assert call(sd=P.BF16) == EDTYPE
+    assert call(hd=7) == EDTYPE
+    assert call(S=12) == EALIGN
+    assert call(s=None) == ENULL
+    assert call(idx=None) == ENULL
+    assert call(h=None) == ENULL
+    assert call(h=FAKE + 2) == EALIGN
+    assert call(Q=0) == OK
+    assert call(S=0) == OK
+
+
+def test_descriptor_layout_matches_header():
+    # int64 x4, three 4-byte enums (+4 padding), int64 x3
+    assert ctypes.sizeof(P.ScanDesc) == 4 * 8 + 3 * 4 + 4 + 3 * 8
+    assert P.ScanDesc.h0_batch_stride.offset == 48

@@ -1,0 +1,123 @@
+"""Parity of precog_retrieve_top1 (bit-exact indices) and precog_inject_gather
+(bit-exact copies) with the oracle, and of the whole query-time path: top-1
+retrieval, injection of the retrieved state, then the query prefill."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_02560_amd import precog as P
+from paper_2608_02560_amd import synth
+from precog_testutil import TOL_BF16, err_rms
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _gpu_top1(q, K):
+    idx = P.top1(q.to(DEV), K.to(DEV))
+    torch.cuda.synchronize()
+    return idx.cpu().numpy()
+
+
+def test_retrieval_workload_bit_exact():
+    """Q=256 queries, M=10000 keys of 384 dims, 32 planted queries."""
+    cfg = synth.RETRIEVAL
+    q, K, pos, rows = synth.retrieval_inputs_host(cfg["Q"], cfg["M"], cfg["E"], cfg["planted"],
+                                                  cfg["seed"])
+    ref, _ = oracle.top1(q, K, nthreads=8)
+    got = _gpu_top1(q, K)
+    assert np.array_equal(got, ref)
+    assert np.array_equal(got[pos.numpy()], rows.numpy().astype(np.int32))
+
+
+@pytest.mark.parametrize("Q,M,E", [(1, 1, 4), (3, 33, 16), (65, 1000, 20), (70, 97, 388),
+                                   (130, 4099, 64), (8, 20000, 1024)])
+def test_retrieval_ragged_shapes(Q, M, E):
+    q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 4), seed=Q * 7 + M + E)
+    ref, _ = oracle.top1(q, K, nthreads=8)
+    assert np.array_equal(_gpu_top1(q, K), ref)
+
+
+def test_retrieval_duplicates_and_near_ties():
+    """Exact duplicate keys resolve to the lowest row; keys that differ from
+    the winner by one fp32 ulp in a few components make fp64 score gaps far
+    below fp32 resolution, so only the exact rescoring can order them."""
+    g = np.random.default_rng(5)
+    q, K, _, _ = synth.retrieval_inputs_host(64, 3000, 384, 0, seed=61)
+    K = K.numpy().copy()
+    qn = q.numpy()
+    win, _ = oracle.top1(qn, K)
+    for i, w in enumerate(win[:32]):
+        base = K[w].copy()
+        # duplicate at a lower and a higher row
+        K[(w + 1) % 3000] = base
+        lo = int(g.integers(0, 3000))
+        # near-tie: nudge 3 components by one ulp towards the query
+        near = base.copy()
+        for c in g.integers(0, 384, 3):
+            near[c] = np.nextafter(near[c], np.float32(np.sign(qn[i, c]) * np.inf))
+        K[lo] = near if i % 2 == 0 else base
+    ref, best = oracle.top1(qn, K, nthreads=8)
+    assert np.array_equal(_gpu_top1(q, torch.from_numpy(K)), ref)
+
+
+def test_retrieval_non_unit_rows_and_empty():
+    q, K, _, _ = synth.retrieval_inputs_host(40, 500, 64, 8, seed=62)
+    scale = torch.from_numpy(np.random.default_rng(1).uniform(0.1, 30.0, (500, 1))).float()
+    K2 = K * scale
+    ref, _ = oracle.top1(q, K2)
+    assert np.array_equal(_gpu_top1(q, K2), ref)
+    empty = _gpu_top1(q, K[:0])
+    assert np.all(empty == -1)
+
+
+@pytest.mark.parametrize("sd,od", [(torch.float16, torch.float16), (torch.float16, torch.float32),
+                                   (torch.float32, torch.float32), (torch.float32, torch.float16)])
+def test_gather_dtypes(sd, od):
+    store = synth.state_store(300, 1024 * 16 + 8, seed=7).to(sd)
+    idx = torch.tensor([5, 0, 299, 5, 17, 299], dtype=torch.int32)
+    h0 = P.gather(store.to(DEV), idx.to(DEV), out_dtype=od)
+    torch.cuda.synchronize()
+    ref = oracle.gather(store, idx.numpy())
+    if od == torch.float16 and sd == torch.float32:
+        ref = oracle.round_f16(ref)
+    assert np.array_equal(h0.double().cpu().numpy(), ref)
+
+
+def test_gather_out_of_range_index_gives_nan_rows():
+    store = synth.state_store(10, 64, seed=8).to(DEV)
+    idx = torch.tensor([3, -1, 10, 9], dtype=torch.int32, device=DEV)
+    h0 = P.gather(store, idx, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.isnan(h0[1]).all() and torch.isnan(h0[2]).all()
+    assert torch.equal(h0[0], store[3].float()) and torch.equal(h0[3], store[9].float())
+
+
+def test_query_time_path_end_to_end():
+    """Retrieve the top-1 state of a 10,000-entry fp16 store (D=1024, N=16),
+    inject it and prefill 32 bf16 query tokens for 256 queries; compare with
+    the oracle doing the same three steps."""
+    cfg = synth.RETRIEVAL
+    wl = synth.QUERY_PREFILL
+    D, N = wl.dim, wl.dstate
+    q, K, pos, rows = synth.retrieval_inputs_host(cfg["Q"], cfg["M"], cfg["E"], cfg["planted"],
+                                                  cfg["seed"])
+    store = synth.state_store(cfg["M"], D * N, seed=33, device=DEV)
+    inp = synth.scan_inputs_host(wl.batch, wl.seqlen, D, N, wl.seed, torch.bfloat16)
+    d = {k: v.to(DEV) for k, v in inp.items()}
+    stream = torch.cuda.current_stream()
+    idx = P.top1(q.to(DEV), K.to(DEV), stream=stream)
+    h0 = P.gather(store, idx, out_dtype=torch.float16, stream=stream).view(wl.batch, D, N)
+    y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0,
+                   out_dtype=torch.float32, state_dtype=torch.float16, stream=stream)
+    torch.cuda.synchronize()
+    ref_idx, _ = oracle.top1(q, K, nthreads=8)
+    assert np.array_equal(idx.cpu().numpy(), ref_idx)
+    h0_ref = oracle.gather(store.cpu(), ref_idx).reshape(wl.batch, D, N)
+    assert np.array_equal(h0.double().cpu().numpy(), h0_ref)
+    y_ref, h_ref = oracle.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                               inp["Dskip"], h0_ref, nthreads=8)
+    assert err_rms(y.double().cpu().numpy(), y_ref) <= TOL_BF16
+    assert err_rms(hT.double().cpu().numpy(), h_ref) <= TOL_BF16

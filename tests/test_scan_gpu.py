@@ -1,0 +1,325 @@
+"""Parity of the HIP scan (precog_scan_encode) with the fp64 oracle.
+
+Small problems are compared element by element over every output; the
+workload-sized ones (corpus encode, long context, large corpus) on sampled
+(b, d) rows that the oracle recomputes independently, in the same launch
+configuration the benchmark times.  Metric: err_rms (max |g - o| over
+max(|o|, rms(o))), bars 1e-5 for fp32 inputs and 2e-3 for bf16 inputs with
+fp32 state; bf16 outputs must sit within one bf16 ulp of the oracle rounded
+to nearest even, fp16 states within one fp16 ulp."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_02560_amd import precog as P
+from paper_2608_02560_amd import synth
+from precog_testutil import TOL_BF16, TOL_F32, err_rms, oracle_rows, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _dev(inp):
+    return {k: (v.to(DEV) if v is not None else None) for k, v in inp.items()}
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _full_oracle(inp, h0=None, want_y=True):
+    return oracle.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                       inp["Dskip"], h0, want_y=want_y, nthreads=8)
+
+
+def _bf16_ulp_ok(got_bf16, ref64):
+    """|got - RNE_bf16(ref)| <= 1 bf16 ulp of the reference."""
+    r = oracle.round_bf16(ref64)
+    g = got_bf16.detach().float().cpu().numpy().astype(np.float64)
+    return np.all(np.abs(g - r) <= oracle.bf16_ulp(r) + 0.0)
+
+
+def _f16_ulp_ok(got_f16, ref64):
+    r = oracle.round_f16(ref64)
+    g = got_f16.detach().float().cpu().numpy().astype(np.float64)
+    _, e = np.frexp(r)
+    ulp = np.ldexp(1.0, np.maximum(e, -13) - 11)
+    return np.all(np.abs(g - r) <= ulp)
+
+
+# ---------------------------------------------------------------------------
+# Single fp32 layer: B=1, L=512, D=128, N=16 (full comparison)
+# ---------------------------------------------------------------------------
+def test_single_layer_fp32_full():
+    wl = synth.SINGLE_LAYER
+    inp = synth.scan_inputs_host(wl.batch, wl.seqlen, wl.dim, wl.dstate, wl.seed, torch.float32)
+    y_ref, h_ref = _full_oracle(inp)
+    d = _dev(inp)
+    for chunk in (0, wl.seqlen, 64, 100, 1):
+        y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"],
+                       chunk=chunk)
+        torch.cuda.synchronize()
+        assert err_rms(_np(y), y_ref) <= TOL_F32, chunk
+        assert err_rms(_np(hT), h_ref) <= TOL_F32, chunk
+
+
+def test_single_layer_split_at_384():
+    """Theorem 1 on the GPU: scan(c ++ q) == scan(q, h0 = hT(c)), split at
+    t = 384 and at points that are not multiples of any tile size."""
+    wl = synth.SINGLE_LAYER
+    inp = synth.scan_inputs_host(wl.batch, wl.seqlen, wl.dim, wl.dstate, wl.seed, torch.float32)
+    y_ref, h_ref = _full_oracle(inp)
+    d = _dev(inp)
+    y_full, h_full = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"])
+    for split in (384, 1, 77, 511):
+        part = lambda t, a, b: t[:, a:b].contiguous()
+        yc, hc = P.scan(part(d["x"], 0, split), part(d["dt"], 0, split), d["A"],
+                        part(d["B"], 0, split), part(d["C"], 0, split),
+                        part(d["z"], 0, split), d["Dskip"])
+        yq, hq = P.scan(part(d["x"], split, None), part(d["dt"], split, None), d["A"],
+                        part(d["B"], split, None), part(d["C"], split, None),
+                        part(d["z"], split, None), d["Dskip"], h0=hc)
+        torch.cuda.synchronize()
+        y_split = torch.cat([yc, yq], dim=1)
+        assert err_rms(_np(hq), h_ref) <= TOL_F32
+        assert err_rms(_np(y_split), y_ref) <= TOL_F32
+        # against the unsplit GPU run: the same recurrence, regrouped
+        assert err_rms(_np(hq), _np(h_full)) <= 1e-6
+        assert err_rms(_np(y_split), _np(y_full)) <= 1e-6
+
+
+def test_split_through_fp16_state_within_paper_bound():
+    """Passing the intermediate state at fp16 (the paper's storage precision)
+    moves the continuation by no more than the rounding of that state,
+    carried forward by the decaying recurrence (App. A floating-point note)."""
+    wl = synth.SINGLE_LAYER
+    inp = synth.scan_inputs_host(wl.batch, wl.seqlen, wl.dim, wl.dstate, wl.seed, torch.float32)
+    d = _dev(inp)
+    s = 384
+    part = lambda t, a, b: t[:, a:b].contiguous()
+    _, hc16 = P.scan(part(d["x"], 0, s), part(d["dt"], 0, s), d["A"], part(d["B"], 0, s),
+                     part(d["C"], 0, s), part(d["z"], 0, s), d["Dskip"],
+                     state_dtype=torch.float16, want_y=False)
+    _, hq = P.scan(part(d["x"], s, None), part(d["dt"], s, None), d["A"], part(d["B"], s, None),
+                   part(d["C"], s, None), part(d["z"], s, None), d["Dskip"], h0=hc16,
+                   state_dtype=torch.float16, want_y=False)
+    _, h_ref = _full_oracle(inp, want_y=False)
+    _, hc_ref = oracle.scan(inp["x"][:, :s], inp["dt"][:, :s], inp["A"], inp["B"][:, :s],
+                            inp["C"][:, :s], want_y=False)
+    torch.cuda.synchronize()
+    # each stored element moves by <= 2^-11 |h| (RNE), and each later step
+    # only shrinks that perturbation (|decay| < 1); the final fp16 store adds
+    # its own 2^-11
+    bound = 2.0 ** -11 * np.max(np.abs(hc_ref)) + 2.0 ** -11 * np.abs(h_ref) + 1e-6
+    assert np.all(np.abs(_np(hq) - h_ref) <= bound)
+
+
+# ---------------------------------------------------------------------------
+# Shapes, options and edge cases (full comparison, small sizes)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("N", [1, 2, 4, 8, 16, 32, 64])
+def test_all_state_sizes(N):
+    inp = synth.scan_inputs_host(2, 37, 72, N, seed=40 + N, in_dtype=torch.float32, h0_std=1.0)
+    y_ref, h_ref = _full_oracle(inp, h0=inp["h0"])
+    d = _dev(inp)
+    y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=d["h0"])
+    torch.cuda.synchronize()
+    assert err_rms(_np(y), y_ref) <= TOL_F32
+    assert err_rms(_np(hT), h_ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("B,L,D", [(1, 1, 8), (3, 5, 8), (2, 129, 200), (1, 300, 264),
+                                   (5, 17, 1032)])
+def test_ragged_shapes(B, L, D):
+    inp = synth.scan_inputs_host(B, L, D, 16, seed=B * 1000 + L + D, in_dtype=torch.float32,
+                                 h0_std=0.5)
+    y_ref, h_ref = _full_oracle(inp, h0=inp["h0"])
+    d = _dev(inp)
+    for chunk in (0, 7, L):
+        y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"],
+                       h0=d["h0"], chunk=chunk)
+        torch.cuda.synchronize()
+        assert err_rms(_np(y), y_ref) <= TOL_F32
+        assert err_rms(_np(hT), h_ref) <= TOL_F32
+
+
+def test_optional_operands():
+    inp = synth.scan_inputs_host(2, 50, 64, 16, seed=51, in_dtype=torch.float32, h0_std=1.0)
+    d = _dev(inp)
+    cases = [dict(z=None), dict(Dskip=None), dict(z=None, Dskip=None), dict(h0=None)]
+    for c in cases:
+        args = dict(z=inp["z"], Dskip=inp["Dskip"], h0=inp["h0"])
+        args.update(c)
+        y_ref, h_ref = oracle.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"],
+                                   args["z"], args["Dskip"], args["h0"])
+        dargs = {k: (v.to(DEV) if v is not None else None) for k, v in args.items()}
+        y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], **dargs)
+        torch.cuda.synchronize()
+        assert err_rms(_np(y), y_ref) <= TOL_F32, c
+        assert err_rms(_np(hT), h_ref) <= TOL_F32, c
+    # state-only encode: y = NULL, C / z / Dskip unread
+    _, h_ref = oracle.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], h0=inp["h0"],
+                           want_y=False)
+    _, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], None, None, None, h0=d["h0"], want_y=False)
+    torch.cuda.synchronize()
+    assert err_rms(_np(hT), h_ref) <= TOL_F32
+
+
+def test_empty_sequence_copies_state():
+    inp = synth.scan_inputs_host(2, 0, 64, 16, seed=52, in_dtype=torch.float32, h0_std=1.0)
+    d = _dev(inp)
+    _, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=d["h0"])
+    _, hz = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"])
+    _, h16 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=d["h0"],
+                    state_dtype=torch.float16)
+    torch.cuda.synchronize()
+    assert torch.equal(hT, d["h0"])
+    assert torch.count_nonzero(hz) == 0
+    assert torch.equal(h16.float(), d["h0"].half().float())
+    # empty batch and empty channel count are no-ops
+    P.scan(d["x"][:0], d["dt"][:0], d["A"], d["B"][:0], d["C"][:0], d["z"][:0], d["Dskip"])
+
+
+def test_in_place_state_and_strided_store():
+    """hT may alias h0 (streaming prefill), and hT may land in a strided slot
+    of a [chunks, layers, D, N] store."""
+    inp = synth.scan_inputs_host(3, 40, 64, 16, seed=53, in_dtype=torch.float32, h0_std=1.0)
+    _, h_ref = _full_oracle(inp, h0=inp["h0"])
+    d = _dev(inp)
+    for chunk in (0, 8):
+        state = d["h0"].clone()
+        P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=state, hT=state,
+               chunk=chunk)
+        torch.cuda.synchronize()
+        assert err_rms(_np(state), h_ref) <= TOL_F32
+    layers = 4
+    store = torch.full((3, layers, 64, 16), -7.0, device=DEV, dtype=torch.float16)
+    h0_16 = inp["h0"].half()
+    _, h_ref16 = _full_oracle(inp, h0=h0_16)
+    for layer in (0, 2):
+        P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0_16.to(DEV),
+               state_dtype=torch.float16, hT=store[:, layer], hT_batch_stride=layers * 64 * 16)
+    torch.cuda.synchronize()
+    assert _f16_ulp_ok(store[:, 0], h_ref16) and _f16_ulp_ok(store[:, 2], h_ref16)
+    assert torch.all(store[:, 1] == -7.0) and torch.all(store[:, 3] == -7.0)
+
+
+def test_fp16_state_io():
+    inp = synth.scan_inputs_host(2, 60, 128, 16, seed=54, in_dtype=torch.float32, h0_std=1.0)
+    h0_16 = inp["h0"].half()
+    y_ref, h_ref = _full_oracle(inp, h0=h0_16)
+    d = _dev(inp)
+    y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"],
+                   h0=h0_16.to(DEV), state_dtype=torch.float16)
+    torch.cuda.synchronize()
+    assert err_rms(_np(y), y_ref) <= TOL_F32
+    assert _f16_ulp_ok(hT, h_ref)
+
+
+def test_deterministic_bitwise():
+    inp = synth.scan_inputs_host(4, 300, 256, 16, seed=55, in_dtype=torch.bfloat16)
+    d = _dev(inp)
+    outs = []
+    for _ in range(2):
+        outs.append(P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"],
+                           out_dtype=torch.bfloat16, state_dtype=torch.float16, chunk=64))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+def test_chunk_sweep_agrees():
+    """Any time-chunk length gives the same result up to fp32 reassociation."""
+    inp = synth.scan_inputs_host(2, 1000, 128, 16, seed=56, in_dtype=torch.bfloat16)
+    y_ref, h_ref = _full_oracle(inp)
+    d = _dev(inp)
+    for chunk in (0, 1000, 999, 256, 64, 33, 8):
+        y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], chunk=chunk)
+        torch.cuda.synchronize()
+        assert err_rms(_np(y), y_ref) <= 1e-5, chunk
+        assert err_rms(_np(hT), h_ref) <= 1e-5, chunk
+
+
+# ---------------------------------------------------------------------------
+# Workload-sized runs, sampled rows
+# ---------------------------------------------------------------------------
+def _device_inputs(wl, need_z_c=True):
+    return synth.scan_inputs_device(wl.batch, wl.seqlen, wl.dim, wl.dstate, wl.seed,
+                                    torch.bfloat16, wl.dt_mu, wl.dt_sigma, DEV,
+                                    need_z_c=need_z_c)
+
+
+def _check_rows(ref, y=None, hT=None, y_tol=TOL_BF16, bf16_y=False, f16_h=False):
+    for (b, d), (yr, hr) in ref.items():
+        if y is not None:
+            if bf16_y:
+                assert _bf16_ulp_ok(y[b, :, d], yr), (b, d)
+            else:
+                assert err_rms(_np(y[b, :, d]), yr) <= y_tol, (b, d)
+        if hT is not None:
+            if f16_h:
+                assert _f16_ulp_ok(hT[b, d], hr), (b, d)
+            else:
+                assert err_rms(_np(hT[b, d]), hr) <= TOL_BF16, (b, d)
+
+
+def test_corpus_encode_full_size_sampled():
+    """B=64, L=3000, D=2048, N=16, bf16 in: fp32 y (parity run) and the timed
+    form (bf16 y, fp16 hT)."""
+    wl = synth.CORPUS_ENCODE
+    inp = _device_inputs(wl)
+    rows = sample_rows(wl.batch, wl.dim, 40, seed=2)
+    ref = oracle_rows(oracle, inp, rows)
+    y, hT = P.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"], inp["Dskip"])
+    torch.cuda.synchronize()
+    _check_rows(ref, y, hT)
+    worst = max(err_rms(_np(y[b, :, d]), r[0]) for (b, d), r in ref.items())
+    print("corpus encode fp32-y err_rms worst %.3e" % worst)
+    del y, hT
+    y16, h16 = P.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], out_dtype=torch.bfloat16, state_dtype=torch.float16)
+    torch.cuda.synchronize()
+    _check_rows(ref, y16, h16, bf16_y=True, f16_h=True)
+
+
+def test_long_context_chunked_sampled():
+    """B=8, L=65536, D=2048, N=16, chunk 256: the inter-chunk carry."""
+    wl = synth.LONG_CONTEXT
+    inp = _device_inputs(wl)
+    rows = sample_rows(wl.batch, wl.dim, 12, seed=4)
+    ref = oracle_rows(oracle, inp, rows)
+    y, hT = P.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"], inp["Dskip"],
+                   chunk=wl.chunk, state_dtype=torch.float32)
+    torch.cuda.synchronize()
+    _check_rows(ref, y, hT)
+    del y, hT
+    y16, h16 = P.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], chunk=wl.chunk, out_dtype=torch.bfloat16,
+                      state_dtype=torch.float16)
+    torch.cuda.synchronize()
+    _check_rows(ref, y16, h16, bf16_y=True, f16_h=True)
+
+
+def test_large_corpus_two_layers_into_store():
+    """B=1024, L=3000, D=1536, N=64, state-only: two of the 24 layers, each
+    writing its final states into its slot of the [1024, 24, D, N] fp16
+    store."""
+    wl = synth.LARGE_CORPUS
+    layers = synth.LARGE_CORPUS_LAYERS
+    D, N = wl.dim, wl.dstate
+    store = torch.zeros((wl.batch, layers, D, N), dtype=torch.float16, device=DEV)
+    for layer in (0, 23):
+        inp = synth.scan_inputs_device(wl.batch, wl.seqlen, D, N, wl.seed + layer,
+                                       torch.bfloat16, wl.dt_mu, wl.dt_sigma, DEV,
+                                       need_z_c=False)
+        P.scan(inp["x"], inp["dt"], inp["A"], inp["B"], None, None, None, want_y=False,
+               state_dtype=torch.float16, hT=store[:, layer],
+               hT_batch_stride=layers * D * N)
+        rows = sample_rows(wl.batch, D, 10, seed=layer)
+        ref = oracle_rows(oracle, inp, rows, want_y=False)
+        torch.cuda.synchronize()
+        for (b, d), (_, hr) in ref.items():
+            assert _f16_ulp_ok(store[b, layer, d], hr), (layer, b, d)
+        del inp
+    assert torch.count_nonzero(store[:, 1:23]) == 0
