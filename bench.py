@@ -25,8 +25,15 @@ if ROOT not in sys.path:
 
 METRIC = "SSM prefill scan tokens/s & achieved HBM GB/s (fraction of peak), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
-# fp32 vector issue rate without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
+# MI355X fp32 vector peak: 157.3 TFLOP/s = 7.86e13 FMA issue slots/s (256 CUs x
+# 2.4 GHz x 128 lanes).  The scan's algorithmic work per (token, channel,
+# state) is 8 issue slots: v_mul (dt A'), v_exp_f32 (quarter rate: 4 slots),
+# v_mul (B x dt), v_fma (state), v_fma (readout); expressed as FMA-equivalent
+# flops (2 per slot) it is 16 per (t, d, n).
+VALU_PEAK_TFLOPS = 157.3
+SLOT_FLOPS_PER_TDN = 16
+PROFILE = os.path.join(ROOT, "profiles", "scan_corpus_encode_b64_l3000_d2048_n16.md")
+SCAN_SOURCE = os.path.join(ROOT, "paper_2608_02560_amd", "csrc", "scan.hip")
 
 
 def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate=True):
@@ -41,6 +48,30 @@ def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate
         total += td * y_bytes + D * 4
     total += B * D * N * st_bytes + D * N * 4
     return total
+
+
+def measured_traffic():
+    """HBM bytes per launch of the corpus-encode scan from the committed
+    rocprofv3 counter summary, or None when the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+
+    try:
+        text = open(PROFILE).read()
+        src = hashlib.sha256(open(SCAN_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("scan.hip sha256") != src:
+        return None
+    try:
+        return float(fields["traffic bytes per launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_threads():
@@ -122,7 +153,7 @@ def bench_corpus(args):
     nbytes = scan_bytes(B, L, D, N)
     tokens = B * L
     achieved = nbytes / (ev_ms * 1e-3) / 1e9
-    valu_ops = 5 * B * L * D * N  # mul, exp2, mul, fma, fma per (t, d, n)
+    alu = SLOT_FLOPS_PER_TDN * B * L * D * N / (ev_ms * 1e-3) / 1e12
     out = {
         "metric": METRIC,
         "value": tokens / (ms * 1e-3),
@@ -141,13 +172,14 @@ def bench_corpus(args):
                    "chunk": args.chunk or "auto", "parallelism": "single GPU"},
         "achieved_gbps": achieved,
         "hbm_frac": achieved / HBM_PEAK_GBPS,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "kernel": "scan_kernel<16, bf16, bf16, fp16, readout>",
-                     "bytes_per_launch": nbytes, "kernel_ms": ev_ms},
-        "alu": {"achieved_ops": valu_ops / (ev_ms * 1e-3), "peak_ops": VALU_PEAK_OPS,
-                "frac": valu_ops / (ev_ms * 1e-3) / VALU_PEAK_OPS,
-                "note": "5 VALU issues per (t,d,n) counted algorithmically"},
+        "roofline": {"bound": "alu", "achieved": alu, "peak": VALU_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": alu / VALU_PEAK_TFLOPS,
+                     "traffic": measured_traffic(),
+                     "kernel": "scan_kernel<16, bf16, bf16, fp16, readout, gate>",
+                     "kernel_ms": ev_ms,
+                     "work": "16 FMA-equivalent flops (8 fp32 issue slots) per (t, d, n)"},
+        "hbm": {"achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBPS, "bytes_per_launch": nbytes},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline_corpus(inp, wl, args.cpu_rows)
@@ -254,8 +286,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--extra", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy (traffic-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the scan, retrieval and injection "
@@ -265,6 +299,16 @@ def main():
     import torch
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy:
+        n = 1 << 30
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n,
+                          "launches": 3}), flush=True)
+        return
     out = bench_corpus(args)
     if args.extra:
         out["extra"] = bench_extra(args)

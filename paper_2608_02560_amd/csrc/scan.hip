@@ -42,7 +42,10 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBlock = 256;  // 4 waves: 256 adjacent channels of one row
-constexpr int kPF = 8;       // time steps of inputs in flight per lane
+#ifndef PRECOG_SCAN_PF
+#define PRECOG_SCAN_PF 8
+#endif
+constexpr int kPF = PRECOG_SCAN_PF;  // time steps of inputs per pipeline tile
 
 enum Kind { kReadout = 0, kStateOnly = 1, kSummary = 2 };
 
@@ -313,14 +316,14 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   auto step = [&](const Tile& tb, int k, int st) {
     const float xv = SI::f32(tb.x[k]);
     const float dtv = SI::f32(tb.dt[k]);
-    float bv[G], cv[G];
+    float cv[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) {
-      bv[j] = SI::f32(tb.b[k][j]);
-      cv[j] = kRead ? SI::f32(tb.c[k][j]) : 0.f;
-    }
+    for (int j = 0; j < G; ++j) cv[j] = kRead ? SI::f32(tb.c[k][j]) : 0.f;
     const float u = dtv * xv;
     float acc = 0.f;
+    float bv[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) bv[j] = SI::f32(tb.b[k][j]);
     token<N, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
     if constexpr (kRead) {
       float out = fmaf(dsk, xv, acc);

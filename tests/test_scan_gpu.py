@@ -172,8 +172,8 @@ def test_empty_sequence_copies_state():
     d = _dev(inp)
     _, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=d["h0"])
     _, hz = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"])
-    _, h16 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=d["h0"],
-                    state_dtype=torch.float16)
+    _, h16 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"],
+                    h0=d["h0"].half(), state_dtype=torch.float16)
     torch.cuda.synchronize()
     assert torch.equal(hT, d["h0"])
     assert torch.count_nonzero(hz) == 0
