@@ -69,7 +69,8 @@ int64_t effective_chunk(const precog_scan_desc* d) {
 // otherwise cut time so that about kTargetWaves waves run.
 int64_t auto_chunk(const precog_scan_desc* d) {
   const int64_t L = d->seqlen;
-  const int64_t waves = d->batch * ceil_div(d->dim, 64);
+  const int64_t lanes_per_channel = d->dstate > 16 ? d->dstate / 16 : 1;
+  const int64_t waves = d->batch * ceil_div(d->dim * lanes_per_channel, 64);
   if (waves >= kTargetWaves || L <= 2 * kMinAutoChunk) return L;
   int64_t nch = ceil_div(kTargetWaves, waves > 0 ? waves : 1);
   const int64_t max_nch = L / kMinAutoChunk;
@@ -158,7 +159,9 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
   if (nchunks > (1LL << 20)) return PRECOG_ERR_SHAPE;
   const ScanWs ws = scan_ws(desc, nchunks);
   if (ws.total > 0 && (!workspace || workspace_bytes < ws.total)) return PRECOG_ERR_WORKSPACE;
-  const int64_t dblocks = ceil_div(D, kBlock);
+  // channels per workgroup: 256 lanes, N / 16 lanes per channel when N > 16
+  const int64_t lanes_per_channel = N > 16 ? N / 16 : 1;
+  const int64_t dblocks = ceil_div(D, kBlock / lanes_per_channel);
   if (dblocks * Bt * nchunks > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   if (Bt * D * N / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
 

@@ -9,7 +9,8 @@
 //   * One lane owns one (b, d) channel and keeps its N state values in VGPRs,
 //     walking a time chunk sequentially.  The 64 lanes of a wave are 64
 //     adjacent channels, so every per-token load of x / dt / z and store of y
-//     is one contiguous 128-byte (bf16) or 256-byte (fp32) segment.
+//     is one contiguous 128-byte (bf16) or 256-byte (fp32) segment.  For
+//     N > 16, N / 16 lanes share a channel, 16 states each.
 //   * B_t and C_t are shared by all channels of a row.  Lane l loads element
 //     16 j + (l mod 16) into register j, so one register holds 16 state
 //     coefficients replicated in each 16-lane DPP row; coefficient n reaches
@@ -211,6 +212,18 @@ __device__ __forceinline__ void token(float (&h)[N], const float (&a2)[N], float
    ...);
 }
 
+// Lanes per channel: N > 16 states are split into groups of 16 held by
+// different lanes, which keeps every lane at 16 states (fewer VGPRs, more
+// resident waves) at the price of a cross-lane sum in the readout.
+template <int N>
+constexpr int kLanesPerChannel = N > 16 ? N / 16 : 1;
+
+// Value held by lane (l xor m) of the wave, through the LDS crossbar.
+__device__ __forceinline__ float lane_xor(float v, int m) {
+  const int src = (static_cast<int>(threadIdx.x & 63) ^ m) * 4;
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, v)));
+}
+
 // One lane = one (b, d) channel over one time chunk.  HASZ: gate present.
 //   KIND == kReadout:   y and (last chunk) hT
 //   KIND == kStateOnly: hT only (y == NULL: C, z, Dskip unread)
@@ -223,7 +236,13 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
     const ScanParams p) {
-  constexpr int G = (N + 15) / 16;  // registers per token for B_t (and C_t)
+  // P lanes share a channel when N > 16, one 16-state group each; group g
+  // occupies DPP rows with (row mod P) == g, so every lane of a row needs the
+  // same coefficients B_t[16 g + m] / C_t[16 g + m] from its row's lane m.
+  constexpr int P = kLanesPerChannel<N>;
+  constexpr int NL = N / P;                // states held by one lane
+  constexpr int G = (NL + 15) / 16;        // registers per token for B_t (and C_t)
+  constexpr int kChan = kBlock / P;        // channels per workgroup
   constexpr bool kRead = KIND == kReadout;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int dblk = lb % p.dblocks;
@@ -231,9 +250,13 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const int b = rest % static_cast<int>(p.B);
   const int c = rest / static_cast<int>(p.B);
   const int64_t D = p.D;
-  const int64_t dwave = static_cast<int64_t>(dblk) * kBlock + (threadIdx.x & ~63);
-  if (dwave >= D) return;  // whole wave past the last channel
-  const int64_t dtrue = static_cast<int64_t>(dblk) * kBlock + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int grp = (lane >> 4) % P;  // this lane's state group
+  // channel of this lane: 16 per row, rows of one channel set are P apart
+  const int64_t wave_d0 = static_cast<int64_t>(dblk) * kChan + wave * (64 / P);
+  if (wave_d0 >= D) return;  // whole wave past the last channel
+  const int64_t dtrue = wave_d0 + (lane & 15) + 16 * (lane / (16 * P));
   const bool live = dtrue < D;
   const int64_t d = live ? dtrue : D - 1;
 
@@ -242,23 +265,24 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const int nsteps = static_cast<int>(t1 > t0 ? t1 - t0 : 0);
 
   // Decay exponents A' = -A log2(e): exp(-dt A) = exp2(dt A').
-  float a2[N];
-  load_state<N>(a2, p.A + d * N);
+  const int64_t sofs = d * N + 16 * grp;  // this lane's states within a [D, N] row
+  float a2[NL];
+  load_state<NL>(a2, p.A + sofs);
 #pragma unroll
-  for (int n = 0; n < N; ++n) a2[n] *= -kLog2e;
+  for (int n = 0; n < NL; ++n) a2[n] *= -kLog2e;
 
-  float h[N];
+  float h[NL];
   if constexpr (KIND == kSummary) {
 #pragma unroll
-    for (int n = 0; n < N; ++n) h[n] = 0.f;
+    for (int n = 0; n < NL; ++n) h[n] = 0.f;
   } else {
     if (p.nchunks > 1) {
-      load_state<N>(h, p.carry + ((static_cast<int64_t>(b) * p.nchunks + c) * D + d) * N);
+      load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
     } else if (p.flags & kHasH0) {
-      load_state<N>(h, static_cast<const TSt*>(p.h0) + b * p.h0_stride + d * N);
+      load_state<NL>(h, static_cast<const TSt*>(p.h0) + b * p.h0_stride + sofs);
     } else {
 #pragma unroll
-      for (int n = 0; n < N; ++n) h[n] = 0.f;
+      for (int n = 0; n < NL; ++n) h[n] = 0.f;
     }
   }
 
@@ -280,9 +304,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const auto rc = make_rsrc(Cg + row0 * N, ns * bc_row);
   const auto ry = make_rsrc(yg + row0 * D, ns * out_row);
   const uint32_t dl = static_cast<uint32_t>(d) * sizeof(TIn);
-  const uint32_t dly = live ? static_cast<uint32_t>(d) * sizeof(TOut) : kDropOffset;
-  const int lane16 = threadIdx.x & 15;
-  const uint32_t el = static_cast<uint32_t>(lane16 < N ? lane16 : N - 1) * sizeof(TIn);
+  // y is written once per channel, by the lanes of group 0.
+  const uint32_t dly = (live && grp == 0) ? static_cast<uint32_t>(d) * sizeof(TOut) : kDropOffset;
+  const int lane16 = lane & 15;
+  const uint32_t el =
+      static_cast<uint32_t>(16 * grp + (lane16 < NL ? lane16 : NL - 1)) * sizeof(TIn);
 
   // Software pipeline over tiles of kPF tokens with two register buffers:
   // while tile i is computed from one buffer, tile i + 1 streams into the
@@ -324,8 +350,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     float bv[G];
 #pragma unroll
     for (int j = 0; j < G; ++j) bv[j] = SI::f32(tb.b[k][j]);
-    token<N, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
+    token<NL, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
     if constexpr (kRead) {
+      // sum the P groups' partial readouts (lanes 16 and 32 apart)
+      if constexpr (P >= 2) acc += lane_xor(acc, 16);
+      if constexpr (P >= 4) acc += lane_xor(acc, 32);
       float out = fmaf(dsk, xv, acc);
       if constexpr (HASZ) {
         const float zv = SI::f32(tb.z[k]);
@@ -364,11 +393,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
 
   if (!live) return;
   if constexpr (KIND == kSummary) {
-    store_state<N>(p.carry + ((static_cast<int64_t>(b) * p.nchunks + c + 1) * D + d) * N, h);
-    p.dtsum[(static_cast<int64_t>(b) * p.nchunks + c) * D + d] = dtacc;
+    store_state<NL>(p.carry + (static_cast<int64_t>(b) * p.nchunks + c + 1) * D * N + sofs, h);
+    if (grp == 0) p.dtsum[(static_cast<int64_t>(b) * p.nchunks + c) * D + d] = dtacc;
   } else {
     if ((p.flags & kHasHT) && c == p.nchunks - 1)
-      store_state<N>(static_cast<TSt*>(p.hT) + b * p.hT_stride + d * N, h);
+      store_state<NL>(static_cast<TSt*>(p.hT) + b * p.hT_stride + sofs, h);
   }
 }
 

@@ -130,10 +130,11 @@ def test_all_state_sizes(N):
     assert err_rms(_np(hT), h_ref) <= TOL_F32
 
 
-@pytest.mark.parametrize("B,L,D", [(1, 1, 8), (3, 5, 8), (2, 129, 200), (1, 300, 264),
-                                   (5, 17, 1032)])
-def test_ragged_shapes(B, L, D):
-    inp = synth.scan_inputs_host(B, L, D, 16, seed=B * 1000 + L + D, in_dtype=torch.float32,
+@pytest.mark.parametrize("B,L,D,N", [(1, 1, 8, 16), (3, 5, 8, 16), (2, 129, 200, 16),
+                                     (1, 300, 264, 16), (5, 17, 1032, 16), (2, 150, 72, 64),
+                                     (3, 77, 40, 32), (1, 200, 264, 64)])
+def test_ragged_shapes(B, L, D, N):
+    inp = synth.scan_inputs_host(B, L, D, N, seed=B * 1000 + L + D + N, in_dtype=torch.float32,
                                  h0_std=0.5)
     y_ref, h_ref = _full_oracle(inp, h0=inp["h0"])
     d = _dev(inp)
