@@ -127,14 +127,17 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E);
  * over the M key rows, the cosine similarity for unit-norm rows.  The result
  * is exact: it equals the argmax of the fp64 inner products summed in index
  * order (products of fp32 values are exact in fp64), ties going to the
- * lowest row.  An fp32 matrix-core screen proposes candidates within a
- * proven error margin and only those are rescored in fp64.
+ * lowest row.  A matrix-core screen (queries and keys split into bf16
+ * high and low parts, three exact products summed in fp32) proposes
+ * candidates within a proven error margin and only those are rescored in
+ * fp64.  Non-finite inputs give unspecified indices.
  *   query_emb  [Q, E] fp32     index_emb [M, E] fp32 (rows of any norm;
  *              the margin scales with the row norms)
  *   idx        [Q] int32 output; M == 0 gives -1
  *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
  *   workspace  precog_retrieve_workspace_bytes(Q, M, E) bytes, 16-byte
- *              aligned. */
+ *              aligned, about 4 Q M + 4 M bytes (the screen scores);
+ *              ceil(M / 32) * ceil(Q / 128) must not exceed 2^31 - 1. */
 precog_status precog_retrieve_top1(const float *query_emb,
                                    const float *index_emb, int64_t Q, int64_t M,
                                    int64_t E, int32_t *idx, void *workspace,

@@ -201,9 +201,31 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 
+namespace {
+// Retrieval workspace: split queries (2 x [nqg, nks, 64] x 16 B), screen
+// scores [Q, 32 nkb], block maxima [Q, nkb], key norms [M] and block norms
+// [nkb], each 256-byte aligned.
+struct RetrieveWs {
+  size_t qsplit, scores, blockmax, rownorm, blocknorm, total;
+};
+RetrieveWs retrieve_ws(int64_t Q, int64_t M, int64_t E) {
+  RetrieveWs w;
+  const size_t nkb = static_cast<size_t>((M + 31) / 32);
+  const size_t nqg = static_cast<size_t>((Q + 127) / 128) * 4;
+  const size_t nks = static_cast<size_t>((E + 15) / 16);
+  w.qsplit = align_up(nqg * nks * 64 * 16);
+  w.scores = align_up(static_cast<size_t>(Q) * nkb * 32 * 4);
+  w.blockmax = align_up(static_cast<size_t>(Q) * nkb * 4);
+  w.rownorm = align_up(static_cast<size_t>(M) * 4);
+  w.blocknorm = align_up(nkb * 4);
+  w.total = 2 * w.qsplit + w.scores + w.blockmax + w.rownorm + w.blocknorm;
+  return w;
+}
+}  // namespace
+
 size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096 || E % 4 != 0) return 0;
-  return align_up(static_cast<size_t>(Q) * M * 4) + align_up(static_cast<size_t>(M) * 4);
+  return retrieve_ws(Q, M, E).total;
 }
 
 precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
@@ -212,6 +234,8 @@ precog_status precog_retrieve_top1(const float* query_emb, const float* index_em
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  // one screen workgroup per (32 keys, 128 queries): the grid must fit an int
+  if (ceil_div(M, 32) * ceil_div(Q, 128) > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   if (Q == 0) return PRECOG_OK;
   if (!query_emb || !idx) return PRECOG_ERR_NULL;
   if (M > 0 && !index_emb) return PRECOG_ERR_NULL;
@@ -224,17 +248,30 @@ precog_status precog_retrieve_top1(const float* query_emb, const float* index_em
   if (st != PRECOG_OK) return st;
 
   precog::RetrieveParams p{};
+  const RetrieveWs w = retrieve_ws(Q, M, E);
+  char* ws = static_cast<char*>(workspace);
   p.q = query_emb;
   p.K = index_emb;
-  p.scores = M > 0 ? static_cast<float*>(workspace) : nullptr;
-  p.rownorm2 = M > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                                align_up(static_cast<size_t>(Q) * M * 4))
-                     : nullptr;
+  if (M > 0) {
+    p.qhi = ws;
+    p.qlo = ws + w.qsplit;
+    char* at = ws + 2 * w.qsplit;
+    p.scores = reinterpret_cast<float*>(at);
+    at += w.scores;
+    p.blockmax = reinterpret_cast<float*>(at);
+    at += w.blockmax;
+    p.rownorm2 = reinterpret_cast<float*>(at);
+    at += w.rownorm;
+    p.blocknorm2 = reinterpret_cast<float*>(at);
+  }
   p.idx = idx;
   p.Q = Q;
   p.M = M;
   p.E = E;
-  p.ld_scores = M;
+  p.nkb = static_cast<int>((M + 31) / 32);
+  p.ld_scores = static_cast<int64_t>(p.nkb) * 32;
+  p.nqg = static_cast<int>((Q + 127) / 128 * 4);
+  p.nks = static_cast<int>((E + 15) / 16);
   (void)hipGetLastError();
   const hipError_t e = precog::launch_retrieve(p, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;

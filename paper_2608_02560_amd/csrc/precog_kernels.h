@@ -48,11 +48,18 @@ hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
 struct RetrieveParams {
   const float* q;      // [Q, E]
   const float* K;      // [M, E]
-  float* scores;       // [Q, M] fp32 screen scores (workspace)
-  float* rownorm2;     // [M] fp32 squared row norms (workspace)
+  void* qhi;           // query bf16 hi parts in operand order (workspace)
+  void* qlo;           // query bf16 lo parts in operand order (workspace)
+  float* scores;       // [Q, ld_scores] screen scores (workspace)
+  float* blockmax;     // [Q, nkb] max screen score per 32-key block (workspace)
+  float* rownorm2;     // [M] squared key norms (workspace)
+  float* blocknorm2;   // [nkb] largest squared key norm per block (workspace)
   int32_t* idx;        // [Q]
   int64_t Q, M, E;
-  int64_t ld_scores;   // row pitch of `scores` in elements
+  int64_t ld_scores;   // row pitch of scores (M rounded up to 32)
+  int nkb;             // ceil(M / 32)
+  int nqg;             // ceil(Q / 128) * 4: 32-query groups, padded to whole workgroups
+  int nks;             // ceil(E / 16): 16-feature steps
 };
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
 
@@ -64,6 +71,15 @@ struct GatherParams {
 };
 hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype,
                          hipStream_t s);
+
+// Raw buffer descriptor over [base, base + bytes): loads at or past `bytes`
+// return zero and stores there are dropped by the hardware range check.
+constexpr int kBufWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
+constexpr uint32_t kDropOffset = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), kBufWord3);
+}
 
 // Maps a hardware workgroup id to a logical one so that logically adjacent
 // workgroups run on the same XCD (the dispatcher deals workgroups to the 8

@@ -2,227 +2,413 @@
 //
 // The answer is defined in fp64: score(q, i) = sum_e q_e k_{i,e} summed in
 // index order (products of fp32 values are exact in fp64), idx = the lowest i
-// attaining the maximum.  Two kernels reach it exactly:
+// attaining the maximum.  Three kernels reach it exactly:
 //
-//   screen   fp32 matrix-core pass (v_mfma_f32_16x16x4_f32): S~ = Q K^T for
-//            every (query, row), plus the squared norm of every key row.
-//   decide   one workgroup per query: m = max_i S~_i at i0, then every row
-//            whose screen score could still be the fp64 maximum,
-//              S~_i + e_i >= m - e_i0,   e_i = g |q| |k_i| + tiny,
-//            is rescored in fp64 in index order, and the best (score, lowest
-//            index) wins.  g bounds the error of any fp32 evaluation order
-//            of an E-term dot product (gamma_E = E u / (1 - E u), u = 2^-24,
-//            with the sum of |q_e k_e| bounded by |q| |k_i| via
-//            Cauchy-Schwarz), inflated to cover the fp32 norms and the fp64
-//            rounding of the reference scores.  The fp64 argmax therefore
-//            always sits in the candidate set, and ties resolve exactly as
-//            in the definition.
+//   prep     splits every query value v into hi = bf16(v) and lo = bf16(v - hi)
+//            (round to nearest even; v - hi is exact in fp32) and stores them
+//            in the order the matrix-core operands are consumed, so a wave's
+//            operand load is one contiguous 1 KiB segment.
+//   screen   workgroup = 32 keys x 128 queries: the keys are read
+//            row-contiguously, split the same way and staged in LDS; each wave
+//            computes a 32 x 32 tile with v_mfma_f32_32x32x16_bf16, summing
+//            q_hi k_hi + q_hi k_lo + q_lo k_hi in fp32 (each product exact).
+//            It stores every screen score S~_i, the maximum of each
+//            (query, 32-key block), and the squared norm of every key and the
+//            largest one of every block.
+//   decide   one wave per query: m = the largest screen score.  A key can
+//            still be the fp64 maximum only if S~_i + e(i) >= m - e(i0), where
+//            e(i) = g |q| |k_i| + tiny bounds the error of its screen score
+//            (g bounds the split error and the fp32 accumulation of the
+//            screen per unit of sum |q_e k_e|, which Cauchy-Schwarz bounds
+//            by |q| |k_i|; it is inflated for the fp32 norms, rounding inside
+//            the matrix core, and the fp64 rounding of the reference).  Blocks
+//            are tested first with their maxima and norm bounds, then the keys
+//            of surviving blocks one by one; every candidate is scored exactly
+//            in fp64 in index order and the best (score, lowest index) wins,
+//            so the result is exact.
 #include "precog_kernels.h"
 
 namespace precog {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRows = 32;   // key rows per screen workgroup
-constexpr int kQW = 64;     // queries per wave pass
-constexpr int kScreenBlock = 256;
+constexpr int kKB = 32;       // keys per block (screen workgroup, block maxima)
+constexpr int kQW = 32;       // queries per wave (one 32 x 32 tile)
+constexpr int kQWG = 4 * kQW; // queries per workgroup
+// features per chunk: the wave preloads its query operands for a whole chunk
+// (2 x kFC / 16 x 4 VGPRs); 128 leaves room for three waves per SIMD
+#ifndef PRECOG_RET_FC
+#define PRECOG_RET_FC 128
+#endif
+constexpr int kFC = PRECOG_RET_FC;
+constexpr int kKS = kFC / 16; // 16-feature MFMA steps per chunk
 
-// Screen: workgroup = kRows key rows x all queries; wave w takes query
-// blocks w, w+4, ...; per pass a wave computes 64 queries x 32 rows as
-// 4 x 2 tiles of 16 x 16.  Within a step of 16 feature indices, lane l
-// (row/col l % 16, slot l / 16) loads a float4 of features
-// [e0 + 4 slot, e0 + 4 slot + 4) and feeds component j to MFMA j: the same
-// permutation of the feature index on both operands leaves the dot product
-// unchanged.
-__global__ __launch_bounds__(kScreenBlock) void screen_kernel(const RetrieveParams p) {
-  const int64_t r0 = static_cast<int64_t>(xcd_remap(blockIdx.x, gridDim.x)) * kRows;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int col = lane & 15;
-  const int slot = lane >> 4;
-  const int64_t E = p.E;
-
-  // Squared norms of this block's rows (fp32, index order).
-  if (threadIdx.x < kRows && r0 + threadIdx.x < p.M) {
-    const float* kr = p.K + (r0 + threadIdx.x) * E;
-    float acc = 0.f;
-    for (int64_t e = 0; e < E; e += 4) {
-      const float4 v = *reinterpret_cast<const float4*>(kr + e);
-      acc = fmaf(v.x, v.x, acc);
-      acc = fmaf(v.y, v.y, acc);
-      acc = fmaf(v.z, v.z, acc);
-      acc = fmaf(v.w, v.w, acc);
-    }
-    p.rownorm2[r0 + threadIdx.x] = acc;
-  }
-
-  // Key rows this lane feeds as the B operand (clamped; results of clamped
-  // rows are never stored).
-  const float* krow[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int64_t r = min(r0 + j * 16 + col, p.M - 1);
-    krow[j] = p.K + r * E;
-  }
-
-  for (int64_t qb = static_cast<int64_t>(wave) * kQW; qb < p.Q; qb += 4 * kQW) {
-    const float* qrow[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t q = min(qb + i * 16 + col, p.Q - 1);
-      qrow[i] = p.q + q * E;
-    }
-    floatx4 acc[4][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    for (int64_t e0 = 0; e0 < E; e0 += 16) {
-      const int64_t e = e0 + 4 * slot;
-      const bool in = e < E;
-      float4 av[4], bv[2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        av[i] = in ? *reinterpret_cast<const float4*>(qrow[i] + e) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bv[j] = in ? *reinterpret_cast<const float4*>(krow[j] + e) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].x, bv[j].x, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].y, bv[j].y, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].z, bv[j].z, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].w, bv[j].w, acc[i][j], 0, 0, 0);
-        }
-    }
-    // Output tile (i, j): lane l holds rows 4 (l / 16) + r (queries) of
-    // column l % 16 (key rows), r = 0..3.
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int64_t key = r0 + j * 16 + col;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t q = qb + i * 16 + 4 * slot + r;
-          if (q < p.Q && key < p.M) p.scores[q * p.ld_scores + key] = acc[i][j][r];
-        }
-      }
-  }
+__device__ __forceinline__ float xor_shfl(float v, int m) {
+  const int src = (static_cast<int>(threadIdx.x & 63) ^ m) * 4;
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, v)));
 }
 
-constexpr int kDecideBlock = 256;
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v += xor_shfl(v, m);
+  return v;
+}
+
+__device__ __forceinline__ void split4(const float4& v, bf16x4& hi, bf16x4& lo) {
+  const floatx4 f = {v.x, v.y, v.z, v.w};
+  hi = __builtin_convertvector(f, bf16x4);
+  lo = __builtin_convertvector(f - __builtin_convertvector(hi, floatx4), bf16x4);
+}
+
+// prep: entry ((g * nks + ks) * 2 + h) * 32 + r holds features
+// [16 ks + 8 h, 16 ks + 8 h + 8) of query 32 g + r (zero past Q or E).
+__global__ __launch_bounds__(256) void prep_kernel(const RetrieveParams p) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t total = static_cast<int64_t>(p.nqg) * p.nks * 64;
+  if (t >= total) return;
+  const int r = static_cast<int>(t & 31);
+  const int h = static_cast<int>((t >> 5) & 1);
+  const int64_t gk = t >> 6;
+  const int ks = static_cast<int>(gk % p.nks);
+  const int64_t g = gk / p.nks;
+  const int64_t q = g * 32 + r;
+  bf16x4 hi[2], lo[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int64_t e = 16 * ks + 8 * h + 4 * c;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (q < p.Q && e < p.E) v = *reinterpret_cast<const float4*>(p.q + q * p.E + e);
+    split4(v, hi[c], lo[c]);
+  }
+  const bf16x8 h8 = {hi[0][0], hi[0][1], hi[0][2], hi[0][3], hi[1][0], hi[1][1], hi[1][2], hi[1][3]};
+  const bf16x8 l8 = {lo[0][0], lo[0][1], lo[0][2], lo[0][3], lo[1][0], lo[1][1], lo[1][2], lo[1][3]};
+  reinterpret_cast<bf16x8*>(p.qhi)[t] = h8;
+  reinterpret_cast<bf16x8*>(p.qlo)[t] = l8;
+}
+
+// screen: workgroup (kb, qg) = key block kb (keys 32 kb + 0..31) x queries
+// [128 qg, 128 qg + 128), wave w taking 32 of them.  Per feature chunk the
+// workgroup loads the block's key rows row-contiguously and every wave its
+// query operands, all before the first wait (one memory latency per chunk);
+// the keys are split and stored in LDS in operand order
+// [ks][h][row], the row index XOR-swizzled with (2 ks + h) so both the
+// staging writes and the operand reads hit distinct banks.  MFMA operands:
+// lane l supplies row / column l mod 32 and the 8 features of half
+// h = l / 32 of the 16-feature step, for queries and keys alike, so each dot
+// product is unchanged whatever order the instruction consumes features in.
+// Output register r holds query row 8 (r / 4) + 4 h + (r mod 4), key column
+// l mod 32; screen scores are stored as 128-byte runs of 32 keys.
+__global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
+  const int nqwg = static_cast<int>((p.Q + kQWG - 1) / kQWG);
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int kb = lb / nqwg;
+  const int qg = lb - kb * nqwg;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  // wave-uniform, so the operand descriptors below live in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r32 = lane & 31;
+  const int half = lane >> 5;
+  const int64_t E = p.E;
+  const int64_t k0 = static_cast<int64_t>(kb) * kKB;
+  const int64_t qw = static_cast<int64_t>(qg) * kQWG + wave * kQW;  // first query of the wave
+  const bool active = qw < p.Q;
+  // its 32-query group in the split layout (clamped for waves past Q, whose
+  // loads stay in bounds and whose results are discarded)
+  const int64_t g = active ? qw / 32 : p.nqg - 1;
+
+  // double-buffered: chunk c is staged in buffer c mod 2, so one barrier per
+  // chunk separates the staging of c from the reads of c - 1 and c - 2
+  __shared__ bf16x8 khi[2][kKS][2][32];
+  __shared__ bf16x8 klo[2][kKS][2][32];
+  __shared__ float nsum[2][kKB];
+
+  const int srow_base = (tid >> 2) & 31;  // key row this thread stages
+  // the block's rows through a descriptor: rows past M read as zero
+  const int64_t nrows = p.M - k0 < kKB ? p.M - k0 : kKB;
+  const __amdgpu_buffer_rsrc_t kres =
+      make_rsrc(p.K + k0 * E, static_cast<uint32_t>(nrows * E * 4));
+  const uint32_t krow_off = static_cast<uint32_t>(srow_base * E * 4);
+  float n2 = 0.f;                         // its share of that row's squared norm
+  // the wave's 32-query group of split operands: nks entries of 1 KiB
+  const uint32_t gbytes = static_cast<uint32_t>(p.nks) * 1024u;
+  const __amdgpu_buffer_rsrc_t hres = make_rsrc(static_cast<const char*>(p.qhi) + g * gbytes, gbytes);
+  const __amdgpu_buffer_rsrc_t lres = make_rsrc(static_cast<const char*>(p.qlo) + g * gbytes, gbytes);
+  const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
+
+  floatx16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+
+  int buf = 0;
+  for (int64_t fc = 0; fc < E; fc += kFC, buf ^= 1) {
+    const int nks = static_cast<int>((E - fc + 15) / 16 < kKS ? (E - fc + 15) / 16 : kKS);
+    const uint32_t ks0 = static_cast<uint32_t>(fc / 16);
+    // issue every load of the chunk before waiting on any: the key float4s
+    // (thread t takes row (t / 4) mod 32 and the float4 columns
+    // t mod 4 + 4 (t / 128) + 8 j, so four lanes read 64 contiguous bytes
+    // of a row and the wave covers 16 rows per load), then the wave's query
+    // operands (entries past the group's nks read as zero)
+    float4 kv[kFC / 32];
+#pragma unroll
+    for (int j = 0; j < kFC / 32; ++j) {
+      const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
+      const int64_t e = fc + 4 * c4;
+      const uint32_t off = e < E ? krow_off + static_cast<uint32_t>(e * 4) : kDropOffset;
+      kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
+    }
+    bf16x8 ah[kKS], al[kKS];
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks) {
+      const uint32_t so = (ks0 + ks) * 1024u;
+      ah[ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(hres, lane_off, so, 0));
+      al[ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(lres, lane_off, so, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < kFC / 32; ++j) {
+      const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
+      const float4 v = kv[j];
+      n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
+      bf16x4 hi, lo;
+      split4(v, hi, lo);
+      const int ks = c4 >> 2;
+      const int h = (c4 >> 1) & 1;
+      const int sub = c4 & 1;
+      const int srow = srow_base ^ ((2 * ks + h) & 31);
+      reinterpret_cast<bf16x4*>(&khi[buf][ks][h][srow])[sub] = hi;
+      reinterpret_cast<bf16x4*>(&klo[buf][ks][h][srow])[sub] = lo;
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int ks = 0; ks < kKS; ++ks) {
+        if (ks < nks) {
+          const int srow = r32 ^ ((2 * ks + half) & 31);
+          const bf16x8 bh = khi[buf][ks][half][srow];
+          const bf16x8 bl = klo[buf][ks][half][srow];
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], bh, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], bl, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[ks], bh, acc, 0, 0, 0);
+        }
+      }
+    }
+  }
+  if (active) {
+    const int64_t key = k0 + r32;
+    const bool key_ok = key < p.M;
+    float mx[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t q = qw + 8 * (r >> 2) + 4 * half + (r & 3);
+      if (q < p.Q && key_ok) p.scores[q * p.ld_scores + key] = acc[r];
+      mx[r] = key_ok ? acc[r] : -INFINITY;
+    }
+    // maximum over the 32 keys (lanes) of each half-wave, step-major so the
+    // 16 shuffles of a step are in flight together
+#pragma unroll
+    for (int m = 1; m < 32; m <<= 1) {
+      float t[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t[r] = xor_shfl(mx[r], m);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], t[r]);
+    }
+    if (r32 == 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t q = qw + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (q < p.Q) p.blockmax[q * p.nkb + kb] = mx[r];
+      }
+    }
+  }
+  // squared key norms (workgroups with qg == 0): the eight threads staging
+  // a row hold disjoint parts of it; combined in a fixed order
+  if (qg == 0) {
+    n2 += xor_shfl(n2, 1);
+    n2 += xor_shfl(n2, 2);
+    if ((tid & 3) == 0) nsum[tid >> 7][srow_base] = n2;
+    __syncthreads();
+    if (tid < kKB) {
+      const float r2 = nsum[0][tid] + nsum[1][tid];
+      const bool ok = k0 + tid < p.M;
+      if (ok) p.rownorm2[k0 + tid] = r2;
+      float mx = ok ? r2 : 0.f;
+      mx = fmaxf(mx, xor_shfl(mx, 1));
+      mx = fmaxf(mx, xor_shfl(mx, 2));
+      mx = fmaxf(mx, xor_shfl(mx, 4));
+      mx = fmaxf(mx, xor_shfl(mx, 8));
+      mx = fmaxf(mx, xor_shfl(mx, 16));
+      if (tid == 0) p.blocknorm2[kb] = mx;
+    }
+  }
+}
 
 __device__ __forceinline__ bool better(double s, int64_t i, double bs, int64_t bi) {
   return bi < 0 || s > bs || (s == bs && i < bi);
 }
 
-// One workgroup per query.
-__global__ __launch_bounds__(kDecideBlock) void decide_kernel(const RetrieveParams p) {
-  const int64_t q = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int64_t E = p.E;
-  const int64_t M = p.M;
-  __shared__ float qs[4096];
-  __shared__ float red_f[kDecideBlock];
-  __shared__ int64_t red_i[kDecideBlock];
-  __shared__ double red_d[kDecideBlock];
+constexpr int kMaxE = 4096;
 
-  const float* qg = p.q + q * E;
-  float nq = 0.f;
-  for (int64_t e = tid; e < E; e += kDecideBlock) {
-    const float v = qg[e];
-    qs[e] = v;
-    nq = fmaf(v, v, nq);
-  }
-  red_f[tid] = nq;
+// fp64 score of key row ii against the query in qs: the wave stages the row
+// in rs, lane 0 sums the exact products in feature order (fma equals
+// multiply-then-add here: the product of two fp32 values is exact in fp64),
+// reading eight float4 pairs per LDS round trip, and every lane gets the sum.
+__device__ __forceinline__ double exact_score(const RetrieveParams& p, const float4* qs, float4* rs,
+                                             int64_t ii, int lane, int E) {
+  const float4* kr = reinterpret_cast<const float4*>(p.K + ii * p.E);
+  __syncthreads();  // previous row consumed (and qs complete)
+#pragma unroll 4
+  for (int e4 = lane; e4 < E / 4; e4 += 64) rs[e4] = kr[e4];
   __syncthreads();
-  for (int w = kDecideBlock / 2; w > 0; w >>= 1) {
-    if (tid < w) red_f[tid] += red_f[tid + w];
-    __syncthreads();
-  }
-  const float qnorm = sqrtf(red_f[0]);
-  __syncthreads();
-
-  // Max screen score and the lowest index attaining it.
-  const float* srow = p.scores + q * p.ld_scores;
-  float m = -INFINITY;
-  int64_t mi = -1;
-  for (int64_t i = tid; i < M; i += kDecideBlock) {
-    const float v = srow[i];
-    if (mi < 0 || v > m) { m = v; mi = i; }
-  }
-  red_f[tid] = m;
-  red_i[tid] = mi;
-  __syncthreads();
-  for (int w = kDecideBlock / 2; w > 0; w >>= 1) {
-    if (tid < w) {
-      const float vo = red_f[tid + w];
-      const int64_t io = red_i[tid + w];
-      if (io >= 0 && (red_i[tid] < 0 || vo > red_f[tid] || (vo == red_f[tid] && io < red_i[tid]))) {
-        red_f[tid] = vo;
-        red_i[tid] = io;
+  double s = 0.0;
+  if (lane == 0) {
+    int e4 = 0;
+    for (; e4 + 8 <= E / 4; e4 += 8) {
+      float4 a[8], b[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        a[j] = qs[e4 + j];
+        b[j] = rs[e4 + j];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        s = fma(static_cast<double>(a[j].x), static_cast<double>(b[j].x), s);
+        s = fma(static_cast<double>(a[j].y), static_cast<double>(b[j].y), s);
+        s = fma(static_cast<double>(a[j].z), static_cast<double>(b[j].z), s);
+        s = fma(static_cast<double>(a[j].w), static_cast<double>(b[j].w), s);
       }
     }
-    __syncthreads();
+    for (; e4 < E / 4; ++e4) {
+      const float4 a = qs[e4];
+      const float4 b = rs[e4];
+      s = fma(static_cast<double>(a.x), static_cast<double>(b.x), s);
+      s = fma(static_cast<double>(a.y), static_cast<double>(b.y), s);
+      s = fma(static_cast<double>(a.z), static_cast<double>(b.z), s);
+      s = fma(static_cast<double>(a.w), static_cast<double>(b.w), s);
+    }
   }
-  const float mmax = red_f[0];
-  const int64_t i0 = red_i[0];
-  __syncthreads();
-  if (i0 < 0) {  // M == 0
-    if (tid == 0) p.idx[q] = -1;
+  const int lo = __builtin_amdgcn_readfirstlane(static_cast<int>(__double2loint(s)));
+  const int hi = __builtin_amdgcn_readfirstlane(static_cast<int>(__double2hiint(s)));
+  return __hiloint2double(hi, lo);
+}
+
+// decide: one 64-lane workgroup per query (see the file comment).  Block
+// maxima and block norm bounds discard whole blocks; in a surviving block
+// each key is tested with its own screen score and norm, and candidates are
+// scored exactly; every lane keeps the same best.
+__global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
+  const int64_t q = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int E = static_cast<int>(p.E);
+  const int nkb = p.nkb;
+  if (nkb == 0) {
+    if (lane == 0) p.idx[q] = -1;
     return;
   }
+  __shared__ float4 qs[kMaxE / 4];
+  __shared__ float4 rs[kMaxE / 4];
+  const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
+  const float* bm = p.blockmax + q * nkb;
+  const float* sc = p.scores + q * p.ld_scores;
 
-  // Error margin of one fp32 screen score (see the file comment).
+  float nq = 0.f;
+#pragma unroll 4
+  for (int e4 = lane; e4 < E / 4; e4 += 64) {
+    const float4 v = qg4[e4];
+    qs[e4] = v;
+    nq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, nq))));
+  }
+  // block maxima and norms, 256 blocks per round trip
+  float m = -INFINITY, nmax = 0.f;
+  for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
+    float b[4], n[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kb = kb0 + 64 * j + lane;
+      b[j] = kb < nkb ? bm[kb] : -INFINITY;
+      n[j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      m = fmaxf(m, b[j]);
+      nmax = fmaxf(nmax, n[j]);
+    }
+  }
+  const float qnorm = sqrtf(wave_sum(nq));
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    m = fmaxf(m, xor_shfl(m, s));
+    nmax = fmaxf(nmax, xor_shfl(nmax, s));
+  }
+
+  // Screen-score error bound per unit of |q| |k_i|: dropped split terms
+  // q_lo k_lo + (q_hi + q_lo) dk + dq k <= 3.05 * 2^-16 (bf16 rounding 2^-8
+  // relative, twice), plus fp32 accumulation of 3E exact products, gamma_3E
+  // (with 1.008 for |hi| + |lo| > |v|); doubled for any rounding the matrix
+  // core performs inside one instruction, the fp32 norms and the fp64
+  // reference's own rounding.
   const double u = 5.9604644775390625e-08;  // 2^-24
-  const double gam = (static_cast<double>(E) * u) / (1.0 - static_cast<double>(E) * u);
-  const double g = gam * 1.001 + 1e-12;
+  const double n3 = 3.0 * static_cast<double>(E);
+  const double gam = (n3 * u) / (1.0 - n3 * u);
+  const double g = 2.0 * (1.008 * gam + 3.05 * 1.52587890625e-05) + 1e-12;
   const double tiny = 1e-30;
-  const double e_i0 = g * static_cast<double>(qnorm) * sqrt(static_cast<double>(p.rownorm2[i0])) + tiny;
-  const double thresh = static_cast<double>(mmax) - e_i0;
+  const double gq = g * static_cast<double>(qnorm);
+  const double thresh = static_cast<double>(m) - (gq * sqrt(static_cast<double>(nmax)) + tiny);
 
   double best = -INFINITY;
   int64_t bi = -1;
-  for (int64_t i = tid; i < M; i += kDecideBlock) {
-    const double ei = g * static_cast<double>(qnorm) * sqrt(static_cast<double>(p.rownorm2[i])) + tiny;
-    if (static_cast<double>(srow[i]) + ei >= thresh) {
-      const float* kr = p.K + i * E;
-      double s = 0.0;
-      for (int64_t e = 0; e < E; ++e)
-        s = s + static_cast<double>(qs[e]) * static_cast<double>(kr[e]);
-      if (better(s, i, best, bi)) { best = s; bi = i; }
+  for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
+    uint64_t bmask[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kb = kb0 + 64 * j + lane;
+      float b = -INFINITY, n = 0.f;
+      if (kb < nkb) {
+        b = bm[kb];
+        n = p.blocknorm2[kb];
+      }
+      const bool pass = kb < nkb && static_cast<double>(b) + gq * sqrt(static_cast<double>(n)) + tiny >= thresh;
+      bmask[j] = __ballot(pass);
     }
-  }
-  red_d[tid] = best;
-  red_i[tid] = bi;
-  __syncthreads();
-  for (int w = kDecideBlock / 2; w > 0; w >>= 1) {
-    if (tid < w) {
-      const double so = red_d[tid + w];
-      const int64_t io = red_i[tid + w];
-      if (io >= 0 && better(so, io, red_d[tid], red_i[tid])) {
-        red_d[tid] = so;
-        red_i[tid] = io;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      while (bmask[j]) {
+        const int blk = kb0 + 64 * j + __builtin_ctzll(bmask[j]);
+        bmask[j] &= bmask[j] - 1;
+        const int64_t i = static_cast<int64_t>(blk) * kKB + (lane & (kKB - 1));
+        bool cand = false;
+        if (lane < kKB && i < p.M)
+          cand = static_cast<double>(sc[i]) + gq * sqrt(static_cast<double>(p.rownorm2[i])) + tiny >= thresh;
+        uint64_t cmask = __ballot(cand);
+        while (cmask) {
+          const int64_t ii = static_cast<int64_t>(blk) * kKB + __builtin_ctzll(cmask);
+          cmask &= cmask - 1;
+          const double s = exact_score(p, qs, rs, ii, lane, E);
+          if (better(s, ii, best, bi)) {
+            best = s;
+            bi = ii;
+          }
+        }
       }
     }
-    __syncthreads();
   }
-  if (tid == 0) p.idx[q] = static_cast<int32_t>(red_i[0]);
+  if (lane == 0) p.idx[q] = static_cast<int32_t>(bi);
 }
 
 }  // namespace
 
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s) {
-  if (p.M > 0) {
-    const int64_t blocks = (p.M + kRows - 1) / kRows;
-    hipLaunchKernelGGL(screen_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kScreenBlock), 0, s, p);
+  if (p.nkb > 0) {
+    const int64_t entries = static_cast<int64_t>(p.nqg) * p.nks * 64;
+    hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, s, p);
+    const int64_t nqwg = (p.Q + kQWG - 1) / kQWG;
+    hipLaunchKernelGGL(screen_kernel, dim3(static_cast<unsigned>(p.nkb * nqwg)), dim3(256), 0, s, p);
   }
-  hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(p.Q)), dim3(kDecideBlock), 0, s, p);
+  hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
   return hipGetLastError();
 }
 

@@ -72,12 +72,6 @@ template <> __device__ __forceinline__ f16_t from_f32<f16_t>(float v) {
 // VGPR + a per-token byte offset in an SGPR, summed by the memory unit, so
 // the time loop spends no VALU work on addresses.  Stores from lanes whose
 // offset is at or past num_records are dropped by the hardware range check.
-constexpr int kBufWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
-constexpr uint32_t kDropOffset = 0x80000000u;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), kBufWord3);
-}
 
 template <typename T> struct Stream;
 template <> struct Stream<float> {
