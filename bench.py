@@ -8,8 +8,9 @@ over the whole batch, inputs resident in HBM.  Prints ONE JSON line.
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--extra]
 
 --extra also times the query-time path (top-1 retrieval, state injection,
-32-token query prefill), the long-context chunked scan and one layer of the
-large corpus encode, reported under "extra".
+32-token query prefill, and its top-3 variant with softmax composition), the
+long-context chunked scan and one layer of the large corpus encode, reported
+under "extra".
 """
 from __future__ import annotations
 
@@ -237,6 +238,30 @@ def bench_extra(args):
         "gather_ms": g_ms, "gather_gbps": 2 * wl.batch * D * N * 2 / (g_ms * 1e-3) / 1e9,
         "prefill_ms": s_ms, "prefill_gbps": sbytes / (s_ms * 1e-3) / 1e9,
         "end_to_end_ms": e_ms,
+    }
+
+    # top-k variant: top-3 retrieval with scores, softmax composition into h0
+    kk = 3
+    idxk = torch.empty((cfg["Q"], kk), dtype=torch.int32, device="cuda")
+    sck = torch.empty((cfg["Q"], kk), dtype=torch.float64, device="cuda")
+    rk_ms = time_events(lambda: P.retrieve_topk(q, K, kk, idxk, sck, ws, nws), 20, flush)
+    P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
+    c_ms = time_events(lambda: P.inject_compose(store, idxk, sck, 1.0, h0.view(wl.batch, -1)), 20,
+                       flush)
+
+    def pipeline_k():
+        P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
+        P.inject_compose(store, idxk, sck, 1.0, h0.view(wl.batch, -1))
+        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], h0, y, hT)
+
+    ek_ms = time_events(pipeline_k, 20, flush)
+    res["query_path_topk"] = {
+        "workload": "as query_path with top-3 retrieval and softmax composition (tau = 1)",
+        "retrieve_topk_ms": rk_ms,
+        "compose_ms": c_ms,
+        "compose_gbps": (kk + 1) * wl.batch * D * N * 2 / (c_ms * 1e-3) / 1e9,
+        "end_to_end_ms": ek_ms,
     }
     del inp, y, hT, h0, store, ws, q, K
     torch.cuda.empty_cache()

@@ -12,6 +12,10 @@
  *                           captured hT (Eq. 1, Sec. 3; capture, Sec. 4.2)
  *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
+ * with the top-k extension of retrieval and injection:
+ *   precog_retrieve_topk    exact top-k with scores (Sec. 4.4, Fig. 1)
+ *   precog_inject_compose   softmax-weighted composition of the top-k states
+ *                           (Sec. 5.4 Eq. smc-fusion)
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are device pointers owned by the caller.  The
@@ -143,6 +147,26 @@ precog_status precog_retrieve_top1(const float *query_emb,
                                    int64_t E, int32_t *idx, void *workspace,
                                    size_t workspace_bytes, void *stream);
 
+/* Top-k retrieval (the top-k extension of Sec. 4.4 and Fig. 1): for each
+ * query q, idx[q, 0..k-1] are the k rows with the largest inner products,
+ * best first, ordered exactly as by the fp64 scores of precog_retrieve_top1
+ * (inner products summed in index order, products exact), ties to the
+ * lower row; score[q, j] is the fp64 score of idx[q, j].  The same screen
+ * and proven margin as precog_retrieve_top1, with the k-th largest block
+ * maximum in place of the maximum, so the result is exact.
+ *   query_emb [Q, E] fp32    index_emb [M, E] fp32
+ *   k         1 <= k <= 64 and k <= M, else PRECOG_ERR_SHAPE
+ *   idx       [Q, k] int32 output
+ *   score     [Q, k] fp64 output, or NULL
+ *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
+ *   workspace precog_retrieve_workspace_bytes(Q, M, E) bytes (the same as
+ *             for top-1).  Non-finite inputs give unspecified indices. */
+precog_status precog_retrieve_topk(const float *query_emb,
+                                   const float *index_emb, int64_t Q, int64_t M,
+                                   int64_t E, int64_t k, int32_t *idx,
+                                   double *score, void *workspace,
+                                   size_t workspace_bytes, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* State injection                                                          */
 /* ------------------------------------------------------------------------ */
@@ -159,6 +183,27 @@ precog_status precog_inject_gather(const void *state_store,
                                    int64_t S, const int32_t *idx, int64_t Q,
                                    void *h0, precog_dtype h0_dtype,
                                    void *stream);
+
+/* Top-k injection (Sec. 5.4 Eq. smc-fusion, the composition of Fig. 1):
+ *   h0[q, :] = sum_{j<k} w_j store[idx[q, j], :],
+ *   w_j = exp(score[q, j] / tau) / sum_i exp(score[q, i] / tau)
+ * The paper's softmax has no temperature: tau = 1 is that formula; other
+ * tau > 0 scale the logits.  Weights are formed in fp64 and rounded once to
+ * fp32; the sum runs in fp32 in rank order (j = 0 first), one fused
+ * multiply-add per term, so each element is within (k + 2) 2^-24
+ * sum_j w_j |h_j| of the exact value (before an fp16 output's rounding).
+ * k = 1 reproduces precog_inject_gather bit for bit.
+ *   store   [M, S] F32 | F16     h0 [Q, S] F32 | F16 (RNE when F16)
+ *   idx     [Q, k] int32 (e.g. from precog_retrieve_topk); a row with any
+ *           index outside [0, M) is filled with NaN
+ *   score   [Q, k] fp64, finite
+ *   1 <= k <= 64; tau > 0 and finite; S % 8 == 0; pointers 16-byte aligned */
+precog_status precog_inject_compose(const void *state_store,
+                                    precog_dtype store_dtype, int64_t M,
+                                    int64_t S, const int32_t *idx,
+                                    const double *score, int64_t Q, int64_t k,
+                                    double tau, void *h0, precog_dtype h0_dtype,
+                                    void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *precog_status_string(precog_status s);

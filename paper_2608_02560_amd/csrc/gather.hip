@@ -1,9 +1,11 @@
-// State injection for gfx950 (query time, Sec. 4.2): h0[q] = store[idx[q]].
+// State injection for gfx950 (query time, Sec. 4.2): h0[q] = store[idx[q]],
+// and its top-k generalisation, the softmax-weighted composition
+// h0[q] = sum_j w_j store[idx[q, j]] (Sec. 5.4 Eq. smc-fusion; Fig. 1).
 //
-// Pure data movement: each lane moves 8 consecutive elements (16 bytes of
-// fp16 or 32 bytes of fp32) so every wave access is a contiguous 1-2 KiB
-// segment.  fp16 -> fp32 widening is exact; fp32 -> fp16 rounds to nearest
-// even.  An index outside [0, M) reads nothing and writes NaN.
+// Each lane moves 8 consecutive elements (16 bytes of fp16 or 32 bytes of
+// fp32) so every wave access is a contiguous 1-2 KiB segment.  fp16 -> fp32
+// widening is exact; fp32 -> fp16 rounds to nearest even.  An index outside
+// [0, M) reads nothing and writes NaN.
 #include "precog_kernels.h"
 
 namespace precog {
@@ -67,6 +69,65 @@ __global__ __launch_bounds__(kBlock) void gather_raw_kernel(const GatherParams p
   reinterpret_cast<uint4*>(p.out)[q * words_per_row + w] = v;
 }
 
+// Composition: wave 0 of each workgroup turns the k scores of its query into
+// weights w_j = exp((s_j - max s) / tau) / sum_i exp((s_i - max s) / tau) in
+// fp64, rounded once to fp32; then every lane sums w_j h_j in fp32 in rank
+// order (j = 0 first), one fma per term.  k = 1 gives w = 1 exactly, so the
+// result equals the plain gather bit for bit.
+template <typename TS, typename TO>
+__global__ __launch_bounds__(kBlock) void compose_kernel(const ComposeParams p) {
+  const int64_t q = blockIdx.y;
+  const int k = p.k;
+  __shared__ float w[kMaxTopK];
+  __shared__ int32_t src[kMaxTopK];
+  __shared__ int bad;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const bool on = lane < k;
+    const double sj = on ? p.score[q * k + lane] : -INFINITY;
+    const int32_t ij = on ? p.idx[q * k + lane] : 0;
+    double mx = sj;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+      const int lo = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2loint(mx)));
+      const int hi = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2hiint(mx)));
+      mx = fmax(mx, __hiloint2double(hi, lo));
+    }
+    const double ej = on ? exp((sj - mx) * p.inv_tau) : 0.0;
+    double tot = ej;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+      const int lo = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2loint(tot)));
+      const int hi = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2hiint(tot)));
+      tot += __hiloint2double(hi, lo);
+    }
+    const bool oob = on && (ij < 0 || ij >= p.M);
+    const uint64_t badmask = __ballot(oob);
+    if (on) {
+      w[lane] = static_cast<float>(ej / tot);
+      src[lane] = ij;
+    }
+    if (lane == 0) bad = badmask != 0;
+  }
+  __syncthreads();
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * kVec;
+  if (e >= p.S) return;
+  float8 acc;
+  if (bad) {
+    const float nan = __builtin_nanf("");
+    acc = float8{nan, nan, nan, nan, nan, nan, nan, nan};
+  } else {
+    acc = float8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < k; ++j) {
+      const float8 v = Vec8<TS>::load(p.store, static_cast<int64_t>(src[j]) * p.S + e);
+      const float wj = w[j];
+#pragma unroll
+      for (int c = 0; c < kVec; ++c) acc[c] = fmaf(wj, v[c], acc[c]);
+    }
+  }
+  Vec8<TO>::store(p.out, q * p.S + e, acc);
+}
+
 }  // namespace
 
 hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype, hipStream_t s) {
@@ -82,6 +143,19 @@ hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype, 
     else
       hipLaunchKernelGGL((gather_kernel<float, f16_t>), grid, dim3(kBlock), 0, s, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_compose(const ComposeParams& p, int store_dtype, int out_dtype, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>((p.S / kVec + kBlock - 1) / kBlock), static_cast<unsigned>(p.Q));
+  if (store_dtype == 2 && out_dtype == 2)
+    hipLaunchKernelGGL((compose_kernel<f16_t, f16_t>), grid, dim3(kBlock), 0, s, p);
+  else if (store_dtype == 2)
+    hipLaunchKernelGGL((compose_kernel<f16_t, float>), grid, dim3(kBlock), 0, s, p);
+  else if (out_dtype == 2)
+    hipLaunchKernelGGL((compose_kernel<float, f16_t>), grid, dim3(kBlock), 0, s, p);
+  else
+    hipLaunchKernelGGL((compose_kernel<float, float>), grid, dim3(kBlock), 0, s, p);
   return hipGetLastError();
 }
 

@@ -3,6 +3,8 @@
 // between host and device or synchronises.
 #include "precog.h"
 
+#include <cmath>
+
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -228,9 +230,10 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E) {
   return retrieve_ws(Q, M, E).total;
 }
 
-precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
-                                   int64_t M, int64_t E, int32_t* idx, void* workspace,
-                                   size_t workspace_bytes, void* stream) {
+namespace {
+precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q, int64_t M,
+                       int64_t E, int64_t k, int32_t* idx, double* score, void* workspace,
+                       size_t workspace_bytes, void* stream) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
@@ -239,7 +242,7 @@ precog_status precog_retrieve_top1(const float* query_emb, const float* index_em
   if (Q == 0) return PRECOG_OK;
   if (!query_emb || !idx) return PRECOG_ERR_NULL;
   if (M > 0 && !index_emb) return PRECOG_ERR_NULL;
-  const void* ptrs[] = {query_emb, index_emb, idx, workspace};
+  const void* ptrs[] = {query_emb, index_emb, idx, workspace, score};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
   const size_t need = precog_retrieve_workspace_bytes(Q, M, E);
@@ -265,6 +268,7 @@ precog_status precog_retrieve_top1(const float* query_emb, const float* index_em
     p.blocknorm2 = reinterpret_cast<float*>(at);
   }
   p.idx = idx;
+  p.score = score;
   p.Q = Q;
   p.M = M;
   p.E = E;
@@ -272,9 +276,26 @@ precog_status precog_retrieve_top1(const float* query_emb, const float* index_em
   p.ld_scores = static_cast<int64_t>(p.nkb) * 32;
   p.nqg = static_cast<int>((Q + 127) / 128 * 4);
   p.nks = static_cast<int>((E + 15) / 16);
+  p.k = static_cast<int>(k);
   (void)hipGetLastError();
   const hipError_t e = precog::launch_retrieve(p, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+}  // namespace
+
+precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
+                                   int64_t M, int64_t E, int32_t* idx, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  return retrieve(query_emb, index_emb, Q, M, E, 1, idx, nullptr, workspace, workspace_bytes,
+                  stream);
+}
+
+precog_status precog_retrieve_topk(const float* query_emb, const float* index_emb, int64_t Q,
+                                   int64_t M, int64_t E, int64_t k, int32_t* idx, double* score,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  if (k < 1 || k > precog::kMaxTopK || k > M) return PRECOG_ERR_SHAPE;
+  return retrieve(query_emb, index_emb, Q, M, E, k, idx, score, workspace, workspace_bytes,
+                  stream);
 }
 
 precog_status precog_inject_gather(const void* state_store, precog_dtype store_dtype, int64_t M,
@@ -307,6 +328,45 @@ precog_status precog_inject_gather(const void* state_store, precog_dtype store_d
     p.Q = (Q - q0) < 65535 ? (Q - q0) : 65535;
     const hipError_t e = precog::launch_gather(p, store_dtype, h0_dtype,
                                                static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return PRECOG_ERR_HIP;
+  }
+  return PRECOG_OK;
+}
+
+precog_status precog_inject_compose(const void* state_store, precog_dtype store_dtype, int64_t M,
+                                    int64_t S, const int32_t* idx, const double* score, int64_t Q,
+                                    int64_t k, double tau, void* h0, precog_dtype h0_dtype,
+                                    void* stream) {
+  if (M < 0 || S < 0 || Q < 0 || k < 1 || k > precog::kMaxTopK) return PRECOG_ERR_SHAPE;
+  if (!(tau > 0.0) || !std::isfinite(tau)) return PRECOG_ERR_SHAPE;
+  if ((store_dtype != PRECOG_F32 && store_dtype != PRECOG_F16) ||
+      (h0_dtype != PRECOG_F32 && h0_dtype != PRECOG_F16))
+    return PRECOG_ERR_DTYPE;
+  if (S % 8 != 0) return PRECOG_ERR_ALIGN;
+  if (Q == 0 || S == 0) return PRECOG_OK;
+  if (!idx || !score || !h0 || (M > 0 && !state_store)) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {state_store, idx, score, h0};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  if (S / 8 / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  (void)hipGetLastError();
+  const int out_bytes = h0_dtype == PRECOG_F32 ? 4 : 2;
+  for (int64_t q0 = 0; q0 < Q; q0 += 65535) {
+    precog::ComposeParams p{};
+    p.store = state_store;
+    p.idx = idx + q0 * k;
+    p.score = score + q0 * k;
+    p.out = static_cast<char*>(h0) + q0 * S * out_bytes;
+    p.M = M;
+    p.S = S;
+    p.Q = (Q - q0) < 65535 ? (Q - q0) : 65535;
+    p.k = static_cast<int>(k);
+    p.inv_tau = 1.0 / tau;
+    const hipError_t e = precog::launch_compose(p, store_dtype, h0_dtype,
+                                                static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return PRECOG_ERR_HIP;
   }
   return PRECOG_OK;

@@ -54,13 +54,16 @@ struct RetrieveParams {
   float* blockmax;     // [Q, nkb] max screen score per 32-key block (workspace)
   float* rownorm2;     // [M] squared key norms (workspace)
   float* blocknorm2;   // [nkb] largest squared key norm per block (workspace)
-  int32_t* idx;        // [Q]
+  int32_t* idx;        // [Q, k]
+  double* score;       // [Q, k] exact scores of idx, or null
   int64_t Q, M, E;
   int64_t ld_scores;   // row pitch of scores (M rounded up to 32)
   int nkb;             // ceil(M / 32)
   int nqg;             // ceil(Q / 128) * 4: 32-query groups, padded to whole workgroups
   int nks;             // ceil(E / 16): 16-feature steps
+  int k;               // keys kept per query, 1..kMaxTopK
 };
+constexpr int kMaxTopK = 64;
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
 
 struct GatherParams {
@@ -71,6 +74,18 @@ struct GatherParams {
 };
 hipError_t launch_gather(const GatherParams& p, int store_dtype, int out_dtype,
                          hipStream_t s);
+
+struct ComposeParams {
+  const void* store;     // [M, S]
+  const int32_t* idx;    // [Q, k]
+  const double* score;   // [Q, k]
+  void* out;             // [Q, S]
+  int64_t M, S, Q;
+  int k;
+  double inv_tau;        // 1 / temperature
+};
+hipError_t launch_compose(const ComposeParams& p, int store_dtype, int out_dtype,
+                          hipStream_t s);
 
 // Raw buffer descriptor over [base, base + bytes): loads at or past `bytes`
 // return zero and stores there are dropped by the hardware range check.

@@ -296,19 +296,36 @@ __device__ __forceinline__ double exact_score(const RetrieveParams& p, const flo
   return __hiloint2double(hi, lo);
 }
 
-// decide: one 64-lane workgroup per query (see the file comment).  Block
-// maxima and block norm bounds discard whole blocks; in a surviving block
-// each key is tested with its own screen score and norm, and candidates are
-// scored exactly; every lane keeps the same best.
+__device__ __forceinline__ double shfl_d(double v, int src_lane) {
+  const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2loint(v)));
+  const int hi = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2hiint(v)));
+  return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ int shfl_i(int v, int src_lane) {
+  return __builtin_amdgcn_ds_bpermute(src_lane * 4, v);
+}
+
+// (value, index) order of the block-maximum pass: larger value first, then
+// lower index.  NaN values are never ranked.
+__device__ __forceinline__ bool before(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+// decide: one 64-lane workgroup per query (see the file comment).  For the
+// k best keys the bound uses t_k, the k-th largest block maximum: k distinct
+// blocks hold a key with screen score >= t_k, so k keys have exact scores
+// >= t_k - e_max and every key of the exact top k has S~_i + e(i) >= that.
+// (k = 1: t_1 = m.)  Blocks are discarded with their maxima and norm bounds,
+// then keys one by one; candidates are scored exactly and kept in a list
+// spread over the lanes (lane j holds rank j), ordered by score, then by
+// lower index.
 __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const int64_t q = blockIdx.x;
   const int lane = threadIdx.x;
   const int E = static_cast<int>(p.E);
   const int nkb = p.nkb;
-  if (nkb == 0) {
-    if (lane == 0) p.idx[q] = -1;
-    return;
-  }
+  const int k = p.k;
   __shared__ float4 qs[kMaxE / 4];
   __shared__ float4 rs[kMaxE / 4];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
@@ -322,28 +339,67 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     qs[e4] = v;
     nq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, nq))));
   }
-  // block maxima and norms, 256 blocks per round trip
-  float m = -INFINITY, nmax = 0.f;
+  // largest block norm, 256 blocks per round trip
+  float nmax = 0.f;
   for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
-    float b[4], n[4];
+    float n[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kb = kb0 + 64 * j + lane;
-      b[j] = kb < nkb ? bm[kb] : -INFINITY;
       n[j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      m = fmaxf(m, b[j]);
-      nmax = fmaxf(nmax, n[j]);
-    }
+    for (int j = 0; j < 4; ++j) nmax = fmaxf(nmax, n[j]);
   }
   const float qnorm = sqrtf(wave_sum(nq));
 #pragma unroll
-  for (int s = 1; s < 64; s <<= 1) {
-    m = fmaxf(m, xor_shfl(m, s));
-    nmax = fmaxf(nmax, xor_shfl(nmax, s));
+  for (int s = 1; s < 64; s <<= 1) nmax = fmaxf(nmax, xor_shfl(nmax, s));
+
+  // t_k: k rounds, each taking the first (value, index) pair after the
+  // previous one; fewer than k ranked blocks leave t_k = -inf (every key is
+  // then a candidate)
+  float tv = INFINITY;
+  int ti = -1;
+  bool found = true;
+  for (int r = 0; r < k && found; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    bool any = false;
+    for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
+      float b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kb = kb0 + 64 * j + lane;
+        b[j] = kb < nkb ? bm[kb] : __builtin_nanf("");
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kb = kb0 + 64 * j + lane;
+        if (before(tv, ti, b[j], kb) && (!any || before(b[j], kb, bv, bi))) {
+          bv = b[j];
+          bi = kb;
+          any = true;
+        }
+      }
+    }
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+      const float ov = xor_shfl(bv, s);
+      const int oi = __builtin_amdgcn_ds_bpermute((lane ^ s) * 4, bi);
+      const bool oany = __builtin_amdgcn_ds_bpermute((lane ^ s) * 4, static_cast<int>(any)) != 0;
+      if (oany && (!any || before(ov, oi, bv, bi))) {
+        bv = ov;
+        bi = oi;
+        any = true;
+      }
+    }
+    found = any;
+    if (any) {
+      tv = bv;
+      ti = bi;
+    }
   }
+  const float tk = found ? tv : -INFINITY;
 
   // Screen-score error bound per unit of |q| |k_i|: dropped split terms
   // q_lo k_lo + (q_hi + q_lo) dk + dq k <= 3.05 * 2^-16 (bf16 rounding 2^-8
@@ -357,10 +413,11 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const double g = 2.0 * (1.008 * gam + 3.05 * 1.52587890625e-05) + 1e-12;
   const double tiny = 1e-30;
   const double gq = g * static_cast<double>(qnorm);
-  const double thresh = static_cast<double>(m) - (gq * sqrt(static_cast<double>(nmax)) + tiny);
+  const double thresh = static_cast<double>(tk) - (gq * sqrt(static_cast<double>(nmax)) + tiny);
 
-  double best = -INFINITY;
-  int64_t bi = -1;
+  // rank list: lane j < k holds the j-th best (score, index) so far
+  double ls = -INFINITY;
+  int64_t li = -1;
   for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
     uint64_t bmask[4];
 #pragma unroll
@@ -388,15 +445,28 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
           const int64_t ii = static_cast<int64_t>(blk) * kKB + __builtin_ctzll(cmask);
           cmask &= cmask - 1;
           const double s = exact_score(p, qs, rs, ii, lane, E);
-          if (better(s, ii, best, bi)) {
-            best = s;
-            bi = ii;
+          // insert at the number of held entries that rank before it
+          const bool ahead = lane < k && li >= 0 && better(ls, li, s, ii);
+          const int pos = __builtin_popcountll(__ballot(ahead));
+          if (pos < k) {
+            const double ps = shfl_d(ls, lane > 0 ? lane - 1 : 0);
+            const int pil = shfl_i(static_cast<int>(li), lane > 0 ? lane - 1 : 0);
+            if (lane > pos) {
+              ls = ps;
+              li = pil;
+            } else if (lane == pos) {
+              ls = s;
+              li = ii;
+            }
           }
         }
       }
     }
   }
-  if (lane == 0) p.idx[q] = static_cast<int32_t>(bi);
+  if (lane < k) {
+    p.idx[q * k + lane] = static_cast<int32_t>(li);
+    if (p.score) p.score[q * k + lane] = ls;
+  }
 }
 
 }  // namespace

@@ -26,7 +26,8 @@ STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECO
 
 EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
-           "precog_inject_gather", "precog_status_string")
+           "precog_retrieve_topk", "precog_inject_gather", "precog_inject_compose",
+           "precog_status_string")
 
 
 class PrecogError(RuntimeError):
@@ -65,9 +66,14 @@ def lib():
         L.precog_retrieve_workspace_bytes.restype = sz
         L.precog_retrieve_top1.argtypes = [vp, vp, i64, i64, i64, vp, vp, sz, vp]
         L.precog_retrieve_top1.restype = ctypes.c_int
+        L.precog_retrieve_topk.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
+        L.precog_retrieve_topk.restype = ctypes.c_int
         L.precog_inject_gather.argtypes = [vp, ctypes.c_int, i64, i64, vp, i64, vp,
                                            ctypes.c_int, vp]
         L.precog_inject_gather.restype = ctypes.c_int
+        L.precog_inject_compose.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, i64,
+                                            ctypes.c_double, vp, ctypes.c_int, vp]
+        L.precog_inject_compose.restype = ctypes.c_int
         L.precog_status_string.argtypes = [ctypes.c_int]
         L.precog_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -132,6 +138,26 @@ def retrieve_top1(query, index, idx, workspace, workspace_bytes=None, stream=Non
     _check("precog_retrieve_top1", st)
 
 
+def retrieve_topk(query, index, k, idx, score, workspace, workspace_bytes=None, stream=None):
+    Q, E = query.shape
+    M = index.shape[0]
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = lib().precog_retrieve_topk(_ptr(query), _ptr(index), Q, M, E, int(k), _ptr(idx),
+                                    _ptr(score), _ptr(workspace), int(workspace_bytes),
+                                    _stream(stream))
+    _check("precog_retrieve_topk", st)
+
+
+def inject_compose(store, idx, score, tau, h0, stream=None):
+    M = store.shape[0]
+    S = store[0].numel() if M > 0 else h0[0].numel()
+    Q, k = idx.shape
+    st = lib().precog_inject_compose(_ptr(store), _DT[store.dtype], M, S, _ptr(idx), _ptr(score),
+                                     Q, k, float(tau), _ptr(h0), _DT[h0.dtype], _stream(stream))
+    _check("precog_inject_compose", st)
+
+
 def inject_gather(store, idx, h0, stream=None):
     M = store.shape[0]
     S = store[0].numel() if M > 0 else h0[0].numel()
@@ -169,6 +195,26 @@ def top1(query, index, stream=None):
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=query.device)
     retrieve_top1(query, index, idx, ws, nbytes, stream)
     return idx
+
+
+def topk(query, index, k, stream=None):
+    """Exact top-k: returns (idx int32 [Q, k], score fp64 [Q, k])."""
+    Q, E = query.shape
+    M = index.shape[0]
+    idx = torch.empty((Q, k), dtype=torch.int32, device=query.device)
+    score = torch.empty((Q, k), dtype=torch.float64, device=query.device)
+    nbytes = retrieve_workspace_bytes(Q, M, E)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=query.device)
+    retrieve_topk(query, index, k, idx, score, ws, nbytes, stream)
+    return idx, score
+
+
+def compose(store, idx, score, tau=1.0, out_dtype=None, stream=None):
+    out_dtype = out_dtype or store.dtype
+    h0 = torch.empty((idx.shape[0],) + tuple(store.shape[1:]), dtype=out_dtype,
+                     device=store.device)
+    inject_compose(store, idx, score, tau, h0, stream)
+    return h0
 
 
 def gather(store, idx, out_dtype=None, stream=None):

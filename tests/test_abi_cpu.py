@@ -115,6 +115,40 @@ def test_retrieve_validation_errors():
     assert call(Q=0) == OK
 
 
+def test_topk_validation_errors():
+    L = P.lib()
+    ws = P.retrieve_workspace_bytes(4, 10, 16)
+    call = lambda q=FAKE, K=FAKE, Q=4, M=10, E=16, k=3, idx=FAKE, sc=FAKE, w=FAKE, wb=ws: \
+        L.precog_retrieve_topk(q, K, Q, M, E, k, idx, sc, w, wb, None)
+    assert call(k=0) == ESHAPE
+    assert call(k=65, M=100) == ESHAPE
+    assert call(k=11) == ESHAPE          # more than M keys
+    assert call(M=0, k=1) == ESHAPE
+    assert call(E=18) == EALIGN
+    assert call(idx=None) == ENULL
+    assert call(sc=FAKE + 8) == EALIGN
+    assert call(w=None) == EWS
+    assert call(Q=0) == OK
+
+
+def test_compose_validation_errors():
+    L = P.lib()
+    call = lambda s=FAKE, sd=P.F16, M=10, S=64, idx=FAKE, sc=FAKE, Q=3, k=3, tau=1.0, h=FAKE, \
+        hd=P.F32: L.precog_inject_compose(s, sd, M, S, idx, sc, Q, k, tau, h, hd, None)
+    assert call(k=0) == ESHAPE
+    assert call(k=65) == ESHAPE
+    assert call(tau=0.0) == ESHAPE
+    assert call(tau=-1.0) == ESHAPE
+    assert call(tau=float("nan")) == ESHAPE
+    assert call(tau=float("inf")) == ESHAPE
+    assert call(sd=P.BF16) == EDTYPE
+    assert call(S=12) == EALIGN
+    assert call(sc=None) == ENULL
+    assert call(idx=None) == ENULL
+    assert call(sc=FAKE + 8) == EALIGN
+    assert call(Q=0) == OK
+
+
 def test_gather_validation_errors():
     L = P.lib()
     call = lambda s=FAKE, sd=P.F16, M=10, S=64, idx=FAKE, Q=3, h=FAKE, hd=P.F32: \

@@ -347,6 +347,36 @@ def test_topk_compose_limits():
     assert np.array_equal(one, oracle.gather(store, idx1))
 
 
+def test_topk_scores_match_sorted_numpy_scores():
+    """Ranks against an independent evaluation: numpy's fp64 matrix product
+    (a different summation order, so only gaps far above fp64 rounding are
+    compared) sorted by (score descending, row ascending)."""
+    q, K, _, _ = synth.retrieval_inputs_host(12, 700, 48, 4, seed=26)
+    idx, sc = oracle.topk_scores(q, K, 7)
+    s = q.double().numpy() @ K.double().numpy().T
+    for i in range(12):
+        order = np.lexsort((np.arange(700), -s[i]))[:7]
+        assert np.array_equal(idx[i], order)
+        assert np.allclose(sc[i], s[i, order], rtol=0, atol=1e-14)
+    # duplicated rows tie exactly and keep row order
+    K2 = torch.cat([K[:5], K[:5]])
+    idx2, sc2 = oracle.topk_scores(q[:3], K2, 10)
+    for i in range(3):
+        assert np.array_equal(sc2[i][0::2], sc2[i][1::2])
+        assert np.all(idx2[i][0::2] < idx2[i][1::2])
+
+
+def test_topk_compose_softmax_by_hand():
+    """Two states, scores 0 and log(3) at tau = 1: weights 1/4 and 3/4."""
+    store = torch.tensor([[1.0, 2.0, 0.0, 8.0], [5.0, -2.0, 4.0, 0.0]])
+    out = oracle.topk_compose(store, np.array([[0, 1]]), np.array([[0.0, np.log(3.0)]]), 1.0)
+    assert np.allclose(out, [[4.0, -1.0, 3.0, 2.0]], rtol=0, atol=1e-15)
+    # temperature halves the logits: log(3)/2 -> weights 1/(1+sqrt3), sqrt3/(1+sqrt3)
+    out2 = oracle.topk_compose(store, np.array([[0, 1]]), np.array([[0.0, np.log(3.0)]]), 2.0)
+    w1 = np.sqrt(3.0) / (1.0 + np.sqrt(3.0))
+    assert np.allclose(out2[0], (1 - w1) * store[0].numpy() + w1 * store[1].numpy(), atol=1e-15)
+
+
 def test_route2_matches_numpy():
     g = np.random.default_rng(8)
     E = 24
