@@ -266,6 +266,29 @@ def bench_extra(args):
     del inp, y, hT, h0, store, ws, q, K
     torch.cuda.empty_cache()
 
+    # SMC trajectory encode at the fidelity dials (state-only, fp16 states)
+    wl = synth.SMC_TRAJECTORY
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, need_z_c=False)
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.F32, P.F16)
+    nws = P.scan_workspace_bytes(desc)
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    traj_res = {"workload": wl.name + ", state-only, fp16 states"}
+    for every in synth.SMC_DIALS:
+        traj = torch.empty((B, L // every, D, N), dtype=torch.float16, device="cuda")
+        run = lambda: P.scan_trajectory(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
+                                        None, None, None, None, traj, every, ws, nws)
+        run()
+        t_ms = time_events(run, 5)
+        nb = scan_bytes(B, L, D, N, readout=False) - B * D * N * 2 + traj.numel() * 2
+        traj_res["every_%d" % every] = {"ms": t_ms, "tokens_per_s": B * L / (t_ms * 1e-3),
+                                        "gbps": nb / (t_ms * 1e-3) / 1e9,
+                                        "states_kept_per_chunk": L // every}
+        del traj
+    res["smc_trajectory"] = traj_res
+    del inp, ws
+    torch.cuda.empty_cache()
+
     # long-context chunked scan (one timed call)
     wl = synth.LONG_CONTEXT
     B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate

@@ -12,7 +12,9 @@
  *                           captured hT (Eq. 1, Sec. 3; capture, Sec. 4.2)
  *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
- * with the top-k extension of retrieval and injection:
+ * with the SMC trajectory variant of the scan:
+ *   precog_scan_trajectory  the scan keeping every k-th state (Sec. 5.1-5.2)
+ * and the top-k extension of retrieval and injection:
  *   precog_retrieve_topk    exact top-k with scores (Sec. 4.4, Fig. 1)
  *   precog_inject_compose   softmax-weighted composition of the top-k states
  *                           (Sec. 5.4 Eq. smc-fusion)
@@ -118,6 +120,29 @@ precog_status precog_scan_encode(const precog_scan_desc *desc, const void *x,
                                  const float *Dskip, const void *h0, void *y,
                                  void *hT, void *workspace,
                                  size_t workspace_bytes, void *stream);
+
+/* precog_scan_encode that also keeps the thinned state trajectory of the SMC
+ * encode (Sec. 5.1 Eq. smc-trajectory, the fidelity dial of Sec. 5.2):
+ *
+ *   traj[b, s, d, n] = h_t[d, n]  for t = every * (s + 1), s = 0..L/every - 1
+ *
+ * i.e. the state after every `every`-th token (t counted from 1).  every = 1
+ * keeps the whole trajectory (K = N_c), every = L only the final state
+ * (K = 1, equal to hT).  All other arguments and outputs are exactly those of
+ * precog_scan_encode (y and hT may be NULL; a state-only trajectory encode
+ * reads x, dt and B only).
+ *   traj   [B, L / every, D, N] in desc->state_dtype (fp16 rounds to nearest
+ *          even), 16-byte aligned; NULL only when L < every (nothing is
+ *          captured then).
+ *   every  >= 1, else PRECOG_ERR_SHAPE. */
+precog_status precog_scan_trajectory(const precog_scan_desc *desc,
+                                     const void *x, const void *dt,
+                                     const float *A, const void *B,
+                                     const void *C, const void *z,
+                                     const float *Dskip, const void *h0,
+                                     void *y, void *hT, void *traj,
+                                     int64_t every, void *workspace,
+                                     size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Cosine top-1 retrieval                                                   */

@@ -139,10 +139,14 @@ size_t precog_scan_workspace_bytes(const precog_scan_desc* desc) {
   return scan_ws(desc, nch).total;
 }
 
-precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, const void* dt,
-                                 const float* A, const void* B, const void* C, const void* z,
-                                 const float* Dskip, const void* h0, void* y, void* hT,
-                                 void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// precog_scan_encode, and with traj != NULL precog_scan_trajectory.
+precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, const float* A,
+                   const void* B, const void* C, const void* z, const float* Dskip,
+                   const void* h0, void* y, void* hT, void* traj, int64_t every, void* workspace,
+                   size_t workspace_bytes, void* stream) {
   precog_status st = validate_desc(desc);
   if (st != PRECOG_OK) return st;
   const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
@@ -151,8 +155,9 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
   if (!A) return PRECOG_ERR_NULL;
   if (work && (!x || !dt || !B)) return PRECOG_ERR_NULL;
   if (work && y && !C) return PRECOG_ERR_NULL;
-  if (!y && !hT) return PRECOG_OK;  // nothing requested
-  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, y, hT, workspace};
+  const int64_t traj_count = traj ? L / every : 0;
+  if (!y && !hT && traj_count == 0) return PRECOG_OK;  // nothing requested
+  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, y, hT, workspace, traj};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
 
@@ -194,13 +199,42 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
   p.dblocks = static_cast<int>(dblocks);
   p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
             (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
-  if (!p.y && !p.hT) return PRECOG_OK;  // L == 0 and no state requested
+  p.traj = traj;
+  p.traj_every = traj ? every : 1;
+  p.traj_count = traj_count;
+  if (!p.y && !p.hT && traj_count == 0) return PRECOG_OK;  // L == 0 and no state requested
 
   (void)hipGetLastError();
-  const hipError_t e = precog::launch_scan(p, static_cast<int>(N), desc->in_dtype,
-                                           desc->out_dtype, desc->state_dtype,
-                                           static_cast<hipStream_t>(stream));
+  const hipError_t e =
+      traj_count > 0
+          ? precog::launch_scan_traj(p, static_cast<int>(N), desc->in_dtype, desc->out_dtype,
+                                     desc->state_dtype, static_cast<hipStream_t>(stream))
+          : precog::launch_scan(p, static_cast<int>(N), desc->in_dtype, desc->out_dtype,
+                                desc->state_dtype, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+}  // namespace
+
+extern "C" {
+
+precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, const void* dt,
+                                 const float* A, const void* B, const void* C, const void* z,
+                                 const float* Dskip, const void* h0, void* y, void* hT,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, y, hT, nullptr, 1, workspace, workspace_bytes,
+              stream);
+}
+
+precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x, const void* dt,
+                                     const float* A, const void* B, const void* C, const void* z,
+                                     const float* Dskip, const void* h0, void* y, void* hT,
+                                     void* traj, int64_t every, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  if (every < 1) return PRECOG_ERR_SHAPE;
+  // traj may be NULL only when nothing would be captured (L < every)
+  if (!traj && desc && desc->seqlen >= every) return PRECOG_ERR_NULL;
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, y, hT, traj, every, workspace,
+              workspace_bytes, stream);
 }
 
 namespace {

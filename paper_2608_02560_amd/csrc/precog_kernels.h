@@ -32,6 +32,8 @@ struct ScanParams {
   void* hT;
   float* carry;   // [B, C, D, N] fp32: slot 0 = h0, slot c = state entering chunk c
   float* dtsum;   // [B, C, D] fp32: slot c = sum of dt over chunk c (c < C-1)
+  void* traj;     // [B, traj_count, D, N] state dtype (trajectory launches only)
+  int64_t traj_every, traj_count;
   int64_t B, L, D;
   int64_t chunk;  // tokens per time chunk
   int64_t h0_stride, hT_stride;
@@ -44,6 +46,8 @@ struct ScanParams {
 // precog_dtype codes of the public header.
 hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
                        int state_dtype, hipStream_t s);
+hipError_t launch_scan_traj(const ScanParams& p, int N, int in_dtype, int out_dtype,
+                            int state_dtype, hipStream_t s);
 
 struct RetrieveParams {
   const float* q;      // [Q, E]

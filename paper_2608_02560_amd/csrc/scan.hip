@@ -1,498 +1,13 @@
-// Gated selective-SSM prefill scan for gfx950 (MI355X).
-//
-// Computes, per batch row b and channel d (Eq. 1, Sec. 3, with real A > 0):
-//   h_t[n] = exp(-dt_t A[n]) h_{t-1}[n] + B_t[n] x_t dt_t
-//   y_t    = (sum_n C_t[n] h_t[n] + Dskip x_t) * silu(z_t)
-// from an injected h0, capturing hT = h_L (Sec. 4.2).
-//
-// Work decomposition (two levels over time):
-//   * One lane owns one (b, d) channel and keeps its N state values in VGPRs,
-//     walking a time chunk sequentially.  The 64 lanes of a wave are 64
-//     adjacent channels, so every per-token load of x / dt / z and store of y
-//     is one contiguous 128-byte (bf16) or 256-byte (fp32) segment.  For
-//     N > 16, N / 16 lanes share a channel, 16 states each.
-//   * B_t and C_t are shared by all channels of a row.  Lane l loads element
-//     16 j + (l mod 16) into register j, so one register holds 16 state
-//     coefficients replicated in each 16-lane DPP row; coefficient n reaches
-//     every lane through the DPP row_newbcast:n operand modifier of the very
-//     instruction that consumes it (v_mul_f32 for B_t[n] x_t dt_t,
-//     v_fmac_f32 for C_t[n] h_t[n]).  The broadcast is free and B_t / C_t
-//     cost 2 N / 16 loads and conversions per lane and token.
-//   * When batch x channels alone cannot fill the 1024 SIMDs, the sequence is
-//     cut into C time chunks (level 2):
-//       pass 1 (summary): each chunk except the last is scanned from a zero
-//              state; its end state and sum of dt are written to workspace;
-//       pass 2 (carry):   per (b, d, n), H_c = exp(-A sum dt_{c-1}) H_{c-1}
-//              + s_{c-1}, sequential over chunks (the composition of the
-//              affine maps h -> a h + s that each chunk applies, App. A);
-//       pass 3 (replay):  each chunk is rescanned from its carried-in state,
-//              producing y and, for the last chunk, hT.
-//     The carried state is exact up to fp32 reassociation (Theorem 1 applied
-//     at every chunk boundary).
-//
-// Per (token, channel, state): one v_mul (dt A'), one v_exp_f32, one
-// v_mul_dpp (B x dt), one v_fmac (state) and one v_fmac_dpp (readout).  A is
-// prescaled by -log2(e) once per lane, so exp(-dt A) = exp2(dt A').  The
-// running state is always fp32.
-#include <utility>
-
-#include "precog_kernels.h"
+// Gated selective-SSM prefill scan (Eq. 1, Sec. 3): the launcher of the
+// plain encode.  The kernels and their design are in scan_kernels.h; the
+// trajectory-capturing variants are instantiated in scan_traj.hip.
+#include "scan_kernels.h"
 
 namespace precog {
-namespace {
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBlock = 256;  // 4 waves: 256 adjacent channels of one row
-#ifndef PRECOG_SCAN_PF
-#define PRECOG_SCAN_PF 8
-#endif
-constexpr int kPF = PRECOG_SCAN_PF;  // time steps of inputs per pipeline tile
-
-enum Kind { kReadout = 0, kStateOnly = 1, kSummary = 2 };
-
-__device__ __forceinline__ float to_f32(float v) { return v; }
-__device__ __forceinline__ float to_f32(bf16_t v) {
-  return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
-}
-__device__ __forceinline__ float to_f32(f16_t v) {
-  return static_cast<float>(__builtin_bit_cast(_Float16, v.bits));
-}
-
-template <typename T> __device__ __forceinline__ T from_f32(float v);
-template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
-template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
-  return bf16_t{__builtin_bit_cast(uint16_t, static_cast<__bf16>(v))};  // RNE
-}
-template <> __device__ __forceinline__ f16_t from_f32<f16_t>(float v) {
-  return f16_t{__builtin_bit_cast(uint16_t, static_cast<_Float16>(v))};  // RNE
-}
-
-// Per-token streams go through buffer instructions: the address is the
-// descriptor base (a wave-uniform row pointer) + a per-lane byte offset in a
-// VGPR + a per-token byte offset in an SGPR, summed by the memory unit, so
-// the time loop spends no VALU work on addresses.  Stores from lanes whose
-// offset is at or past num_records are dropped by the hardware range check.
-
-template <typename T> struct Stream;
-template <> struct Stream<float> {
-  using raw = uint32_t;
-  static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
-  }
-  static __device__ __forceinline__ float f32(raw v) { return __uint_as_float(v); }
-  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float v) {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
-  }
-};
-template <> struct Stream<bf16_t> {
-  using raw = uint16_t;
-  static __device__ __forceinline__ raw load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
-  }
-  static __device__ __forceinline__ float f32(raw v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
-  static __device__ __forceinline__ void store(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float v) {
-    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, static_cast<__bf16>(v)), r, voff, soff, 0);
-  }
-};
-
-template <int N, typename TSt>
-__device__ __forceinline__ void load_state(float (&h)[N], const TSt* src) {
-#pragma unroll
-  for (int n = 0; n < N; ++n) h[n] = to_f32(src[n]);
-}
-template <int N>
-__device__ __forceinline__ void load_state(float (&h)[N], const float* src) {
-  if constexpr (N % 4 == 0) {
-#pragma unroll
-    for (int n = 0; n < N; n += 4) {
-      const float4 v = *reinterpret_cast<const float4*>(src + n);
-      h[n] = v.x; h[n + 1] = v.y; h[n + 2] = v.z; h[n + 3] = v.w;
-    }
-  } else {
-#pragma unroll
-    for (int n = 0; n < N; ++n) h[n] = src[n];
-  }
-}
-
-template <int N, typename TSt>
-__device__ __forceinline__ void store_state(TSt* dst, const float (&h)[N]) {
-#pragma unroll
-  for (int n = 0; n < N; ++n) dst[n] = from_f32<TSt>(h[n]);
-}
-template <int N>
-__device__ __forceinline__ void store_state(float* dst, const float (&h)[N]) {
-  if constexpr (N % 4 == 0) {
-#pragma unroll
-    for (int n = 0; n < N; n += 4)
-      *reinterpret_cast<float4*>(dst + n) = make_float4(h[n], h[n + 1], h[n + 2], h[n + 3]);
-  } else {
-#pragma unroll
-    for (int n = 0; n < N; ++n) dst[n] = h[n];
-  }
-}
-
-// Value of lane 16 r + m broadcast to all 16 lanes of DPP row r.  The
-// compiler folds the move into the consuming v_mul_f32 as a DPP operand.
-template <int m>
-__device__ __forceinline__ float row_bcast(float v) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x150 + m, 0xf, 0xf, false));
-}
-
-// Same broadcast for a lane chosen at run time (short groups, N < 16).
-__device__ __forceinline__ float row_bcast_rt(float v, int m) {
-  const int src = (static_cast<int>(threadIdx.x) & 48) + m;  // lane 16 r + m, r = row of this lane
-  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src * 4, __builtin_bit_cast(int, v)));
-}
-
-// acc += sum_m bcast_m(c) h[16 g + m] over the states of group g, each term
-// one v_fmac_f32 with the broadcast as its DPP operand.  The compiler does
-// not form v_fmac_f32_dpp itself, so the group is one asm block (one block
-// rather than one statement per term: the hazard recognizer pads every asm
-// statement conservatively).  Inside the block the DPP source `c` is never
-// written; it was last written by a VALU conversion before the block, and a
-// DPP source needs two wait states after a VALU write, hence s_nop 1.
-template <int N, int g>
-__device__ __forceinline__ void readout_group(float& acc, float c, const float (&h)[N]) {
-  constexpr int kPer = N < 16 ? N : 16;
-  constexpr int o = 16 * g;
-  if constexpr (kPer == 16) {
-    asm("s_nop 1\n\t"
-        "v_fmac_f32_dpp %0, %1, %2 row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %3 row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %4 row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %5 row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %6 row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %7 row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %8 row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %9 row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %10 row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %11 row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %12 row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %13 row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %14 row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %15 row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %16 row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
-        "v_fmac_f32_dpp %0, %1, %17 row_newbcast:15 row_mask:0xf bank_mask:0xf"
-        : "+v"(acc)
-        : "v"(c), "v"(h[o + 0]), "v"(h[o + 1]), "v"(h[o + 2]), "v"(h[o + 3]), "v"(h[o + 4]),
-          "v"(h[o + 5]), "v"(h[o + 6]), "v"(h[o + 7]), "v"(h[o + 8]), "v"(h[o + 9]),
-          "v"(h[o + 10]), "v"(h[o + 11]), "v"(h[o + 12]), "v"(h[o + 13]), "v"(h[o + 14]),
-          "v"(h[o + 15]));
-  } else {
-    // N < 16: short groups, one statement per term (only small test shapes).
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) acc = fmaf(row_bcast_rt(c, m), h[o + m], acc);
-  }
-}
-
-// One token for the 16 states n = 16 g + m, m = 0..15 (or fewer when N < 16).
-template <int N, bool READOUT, int g, int... m>
-__device__ __forceinline__ void token_group(float (&h)[N], const float (&a2)[N], float dtv, float u,
-                                            float bv, float cv, float& acc,
-                                            std::integer_sequence<int, m...>) {
-  ((h[16 * g + m] = fmaf(__builtin_amdgcn_exp2f(dtv * a2[16 * g + m]), h[16 * g + m],
-                         u * row_bcast<m>(bv))),
-   ...);
-  if constexpr (READOUT) readout_group<N, g>(acc, cv, h);
-}
-
-template <int N, bool READOUT, int... g>
-__device__ __forceinline__ void token(float (&h)[N], const float (&a2)[N], float dtv, float u,
-                                      const float (&bv)[(N + 15) / 16], const float (&cv)[(N + 15) / 16],
-                                      float& acc, std::integer_sequence<int, g...>) {
-  constexpr int kPer = N < 16 ? N : 16;
-  (token_group<N, READOUT, g>(h, a2, dtv, u, bv[g], cv[g], acc, std::make_integer_sequence<int, kPer>{}),
-   ...);
-}
-
-// Lanes per channel: N > 16 states are split into groups of 16 held by
-// different lanes, which keeps every lane at 16 states (fewer VGPRs, more
-// resident waves) at the price of a cross-lane sum in the readout.
-template <int N>
-constexpr int kLanesPerChannel = N > 16 ? N / 16 : 1;
-
-// Value held by lane (l xor m) of the wave, through the LDS crossbar.
-__device__ __forceinline__ float lane_xor(float v, int m) {
-  const int src = (static_cast<int>(threadIdx.x & 63) ^ m) * 4;
-  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, v)));
-}
-
-// One lane = one (b, d) channel over one time chunk.  HASZ: gate present.
-//   KIND == kReadout:   y and (last chunk) hT
-//   KIND == kStateOnly: hT only (y == NULL: C, z, Dskip unread)
-//   KIND == kSummary:   chunk end state from zero -> carry slot c+1, sum dt
-// Every lane of a wave stays active through the time loop (DPP broadcasts
-// read other lanes); lanes past D compute on clamped channels and store
-// nothing.
-template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ>
-__global__ __launch_bounds__(kBlock) void scan_kernel(
-    const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
-    const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
-    const ScanParams p) {
-  // P lanes share a channel when N > 16, one 16-state group each; group g
-  // occupies DPP rows with (row mod P) == g, so every lane of a row needs the
-  // same coefficients B_t[16 g + m] / C_t[16 g + m] from its row's lane m.
-  constexpr int P = kLanesPerChannel<N>;
-  constexpr int NL = N / P;                // states held by one lane
-  constexpr int G = (NL + 15) / 16;        // registers per token for B_t (and C_t)
-  constexpr int kChan = kBlock / P;        // channels per workgroup
-  constexpr bool kRead = KIND == kReadout;
-  const int lb = xcd_remap(blockIdx.x, gridDim.x);
-  const int dblk = lb % p.dblocks;
-  const int rest = lb / p.dblocks;
-  const int b = rest % static_cast<int>(p.B);
-  const int c = rest / static_cast<int>(p.B);
-  const int64_t D = p.D;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int grp = (lane >> 4) % P;  // this lane's state group
-  // channel of this lane: 16 per row, rows of one channel set are P apart
-  const int64_t wave_d0 = static_cast<int64_t>(dblk) * kChan + wave * (64 / P);
-  if (wave_d0 >= D) return;  // whole wave past the last channel
-  const int64_t dtrue = wave_d0 + (lane & 15) + 16 * (lane / (16 * P));
-  const bool live = dtrue < D;
-  const int64_t d = live ? dtrue : D - 1;
-
-  const int64_t t0 = static_cast<int64_t>(c) * p.chunk;
-  const int64_t t1 = min(p.L, t0 + p.chunk);
-  const int nsteps = static_cast<int>(t1 > t0 ? t1 - t0 : 0);
-
-  // Decay exponents A' = -A log2(e): exp(-dt A) = exp2(dt A').
-  const int64_t sofs = d * N + 16 * grp;  // this lane's states within a [D, N] row
-  float a2[NL];
-  load_state<NL>(a2, p.A + sofs);
-#pragma unroll
-  for (int n = 0; n < NL; ++n) a2[n] *= -kLog2e;
-
-  float h[NL];
-  if constexpr (KIND == kSummary) {
-#pragma unroll
-    for (int n = 0; n < NL; ++n) h[n] = 0.f;
-  } else {
-    if (p.nchunks > 1) {
-      load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
-    } else if (p.flags & kHasH0) {
-      load_state<NL>(h, static_cast<const TSt*>(p.h0) + b * p.h0_stride + sofs);
-    } else {
-#pragma unroll
-      for (int n = 0; n < NL; ++n) h[n] = 0.f;
-    }
-  }
-
-  const float dsk = (kRead && (p.flags & kHasD)) ? p.Dskip[d] : 0.f;
-
-  // Descriptors over this chunk's rows of x, dt, z, y ([nsteps, D]) and
-  // B, C ([nsteps, N]); lane offsets in bytes.
-  using SI = Stream<TIn>;
-  using SO = Stream<TOut>;
-  const int64_t row0 = static_cast<int64_t>(b) * p.L + t0;  // token index of t0
-  const uint32_t in_row = static_cast<uint32_t>(D * sizeof(TIn));   // bytes per token
-  const uint32_t out_row = static_cast<uint32_t>(D * sizeof(TOut));
-  const uint32_t bc_row = static_cast<uint32_t>(N * sizeof(TIn));
-  const uint32_t ns = static_cast<uint32_t>(nsteps > 0 ? nsteps : 1);
-  const auto rx = make_rsrc(xg + row0 * D, ns * in_row);
-  const auto rd = make_rsrc(dtg + row0 * D, ns * in_row);
-  const auto rz = make_rsrc(zg + row0 * D, ns * in_row);
-  const auto rb = make_rsrc(Bg + row0 * N, ns * bc_row);
-  const auto rc = make_rsrc(Cg + row0 * N, ns * bc_row);
-  const auto ry = make_rsrc(yg + row0 * D, ns * out_row);
-  const uint32_t dl = static_cast<uint32_t>(d) * sizeof(TIn);
-  // y is written once per channel, by the lanes of group 0.
-  const uint32_t dly = (live && grp == 0) ? static_cast<uint32_t>(d) * sizeof(TOut) : kDropOffset;
-  const int lane16 = lane & 15;
-  const uint32_t el =
-      static_cast<uint32_t>(16 * grp + (lane16 < NL ? lane16 : NL - 1)) * sizeof(TIn);
-
-  // Software pipeline over tiles of kPF tokens with two register buffers:
-  // while tile i is computed from one buffer, tile i + 1 streams into the
-  // other.  Each buffer keeps fixed registers (no rotation), and a buffer is
-  // refilled only after its tile has been consumed.  Tiles past the chunk
-  // reread its last token (in bounds, never used), so loads need no guards.
-  struct Tile {
-    typename SI::raw x[kPF], dt[kPF], z[kPF], b[kPF][G], c[kPF][G];
-  };
-  Tile t0b, t1b;
-  const int last = nsteps > 0 ? nsteps - 1 : 0;
-  auto fetch = [&](Tile& tb, int tile) {
-#pragma unroll
-    for (int k = 0; k < kPF; ++k) {
-      int st = tile * kPF + k;
-      st = st < last ? st : last;
-      const uint32_t so = static_cast<uint32_t>(st) * in_row;
-      tb.x[k] = SI::load(rx, dl, so);
-      tb.dt[k] = SI::load(rd, dl, so);
-      if constexpr (HASZ) tb.z[k] = SI::load(rz, dl, so);
-      const uint32_t sb = static_cast<uint32_t>(st) * bc_row;
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        tb.b[k][j] = SI::load(rb, el + 16 * j * sizeof(TIn), sb);
-        if constexpr (kRead) tb.c[k][j] = SI::load(rc, el + 16 * j * sizeof(TIn), sb);
-      }
-    }
-  };
-
-  float dtacc = 0.f;
-  auto step = [&](const Tile& tb, int k, int st) {
-    const float xv = SI::f32(tb.x[k]);
-    const float dtv = SI::f32(tb.dt[k]);
-    float cv[G];
-#pragma unroll
-    for (int j = 0; j < G; ++j) cv[j] = kRead ? SI::f32(tb.c[k][j]) : 0.f;
-    const float u = dtv * xv;
-    float acc = 0.f;
-    float bv[G];
-#pragma unroll
-    for (int j = 0; j < G; ++j) bv[j] = SI::f32(tb.b[k][j]);
-    token<NL, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
-    if constexpr (kRead) {
-      // sum the P groups' partial readouts (lanes 16 and 32 apart)
-      if constexpr (P >= 2) acc += lane_xor(acc, 16);
-      if constexpr (P >= 4) acc += lane_xor(acc, 32);
-      float out = fmaf(dsk, xv, acc);
-      if constexpr (HASZ) {
-        const float zv = SI::f32(tb.z[k]);
-        const float e = __builtin_amdgcn_exp2f(-kLog2e * zv);
-        out *= zv * __builtin_amdgcn_rcpf(1.f + e);
-      }
-      SO::store(ry, dly, static_cast<uint32_t>(st) * out_row, out);
-    }
-    if constexpr (KIND == kSummary) dtacc += dtv;
-  };
-  auto run_tile = [&](const Tile& tb, int tile) {
-#pragma unroll
-    for (int k = 0; k < kPF; ++k) step(tb, k, tile * kPF + k);
-  };
-  auto run_tile_guarded = [&](const Tile& tb, int tile) {
-#pragma unroll
-    for (int k = 0; k < kPF; ++k)
-      if (tile * kPF + k < nsteps) step(tb, k, tile * kPF + k);
-  };
-
-  if (nsteps > 0) {
-    fetch(t0b, 0);
-    int tile = 0;
-    // Pairs of whole tiles: straight-line code, no per-token guards.
-    for (; (tile + 2) * kPF <= nsteps; tile += 2) {
-      fetch(t1b, tile + 1);
-      run_tile(t0b, tile);
-      fetch(t0b, tile + 2);
-      run_tile(t1b, tile + 1);
-    }
-    // Fewer than 2 kPF tokens remain: tile `tile` is in t0b.
-    fetch(t1b, tile + 1);
-    run_tile_guarded(t0b, tile);
-    run_tile_guarded(t1b, tile + 1);
-  }
-
-  if (!live) return;
-  if constexpr (KIND == kSummary) {
-    store_state<NL>(p.carry + (static_cast<int64_t>(b) * p.nchunks + c + 1) * D * N + sofs, h);
-    if (grp == 0) p.dtsum[(static_cast<int64_t>(b) * p.nchunks + c) * D + d] = dtacc;
-  } else {
-    if ((p.flags & kHasHT) && c == p.nchunks - 1)
-      store_state<NL>(static_cast<TSt*>(p.hT) + b * p.hT_stride + sofs, h);
-  }
-}
-
-// Pass 2: per (b, d, n) lane, fold the chunk summaries in time order.
-// carry[b, 0] = h0; carry[b, c] = exp2(A' S_{c-1}) carry[b, c-1] + s_{c-1},
-// where pass 1 left s_{c-1} in carry[b, c] and S_{c-1} in dtsum[b, c-1].
-template <typename TSt>
-__global__ __launch_bounds__(256) void carry_kernel(const ScanParams p, int N) {
-  const int64_t DN = p.D * N;
-  const int64_t gid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (gid >= p.B * DN) return;
-  const int64_t b = gid / DN;
-  const int64_t dn = gid - b * DN;
-  const int64_t d = dn / N;
-  const float a2 = -kLog2e * p.A[dn];
-  float H = (p.flags & kHasH0) ? to_f32(static_cast<const TSt*>(p.h0)[b * p.h0_stride + dn]) : 0.f;
-  float* cp = p.carry + b * p.nchunks * DN + dn;
-  const float* sp = p.dtsum + b * p.nchunks * p.D + d;
-  cp[0] = H;
-  constexpr int kU = 8;
-  for (int c0 = 1; c0 < p.nchunks; c0 += kU) {
-    float sv[kU], Sv[kU];
-#pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      if (c0 + k < p.nchunks) {
-        sv[k] = cp[(c0 + k) * DN];
-        Sv[k] = sp[(c0 + k - 1) * p.D];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < kU; ++k) {
-      if (c0 + k < p.nchunks) {
-        H = fmaf(__builtin_amdgcn_exp2f(a2 * Sv[k]), H, sv[k]);
-        cp[(c0 + k) * DN] = H;
-      }
-    }
-  }
-}
-
-template <int N, typename TIn, typename TOut, typename TSt>
-hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
-  const int64_t rows_blocks = static_cast<int64_t>(p.dblocks) * p.B;
-  const TIn* X = static_cast<const TIn*>(p.x);
-  const TIn* DT = static_cast<const TIn*>(p.dt);
-  const TIn* Z = static_cast<const TIn*>(p.z);
-  const TIn* BB = static_cast<const TIn*>(p.Bm);
-  const TIn* CC = static_cast<const TIn*>(p.Cm);
-  if (p.nchunks > 1) {
-    const int64_t g1 = rows_blocks * (p.nchunks - 1);
-    hipLaunchKernelGGL((scan_kernel<N, TIn, float, float, kSummary, false>), dim3(static_cast<unsigned>(g1)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
-    const int64_t lanes = p.B * p.D * N;
-    hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
-                       0, s, p, N);
-  }
-  const int64_t g3 = rows_blocks * p.nchunks;
-  if (p.y != nullptr && (p.flags & kHasZ))
-    hipLaunchKernelGGL((scan_kernel<N, TIn, TOut, TSt, kReadout, true>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
-  else if (p.y != nullptr)
-    hipLaunchKernelGGL((scan_kernel<N, TIn, TOut, TSt, kReadout, false>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
-  else
-    hipLaunchKernelGGL((scan_kernel<N, TIn, float, TSt, kStateOnly, false>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
-  return hipGetLastError();
-}
-
-template <int N, typename TIn, typename TOut>
-hipError_t pick_state(const ScanParams& p, int state_dtype, hipStream_t s) {
-  return state_dtype == 0 ? launch_typed<N, TIn, TOut, float>(p, s)
-                          : launch_typed<N, TIn, TOut, f16_t>(p, s);
-}
-
-template <int N, typename TIn>
-hipError_t pick_out(const ScanParams& p, int out_dtype, int state_dtype, hipStream_t s) {
-  return out_dtype == 0 ? pick_state<N, TIn, float>(p, state_dtype, s)
-                        : pick_state<N, TIn, bf16_t>(p, state_dtype, s);
-}
-
-template <int N>
-hipError_t pick_in(const ScanParams& p, int in_dtype, int out_dtype, int state_dtype,
-                   hipStream_t s) {
-  return in_dtype == 0 ? pick_out<N, float>(p, out_dtype, state_dtype, s)
-                       : pick_out<N, bf16_t>(p, out_dtype, state_dtype, s);
-}
-
-}  // namespace
 
 hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
                        int state_dtype, hipStream_t s) {
-  switch (N) {
-    case 1: return pick_in<1>(p, in_dtype, out_dtype, state_dtype, s);
-    case 2: return pick_in<2>(p, in_dtype, out_dtype, state_dtype, s);
-    case 4: return pick_in<4>(p, in_dtype, out_dtype, state_dtype, s);
-    case 8: return pick_in<8>(p, in_dtype, out_dtype, state_dtype, s);
-    case 16: return pick_in<16>(p, in_dtype, out_dtype, state_dtype, s);
-    case 32: return pick_in<32>(p, in_dtype, out_dtype, state_dtype, s);
-    case 64: return pick_in<64>(p, in_dtype, out_dtype, state_dtype, s);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_scan_n<false>(p, N, in_dtype, out_dtype, state_dtype, s);
 }
 
 }  // namespace precog

@@ -24,7 +24,7 @@ STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECO
           4: "PRECOG_ERR_STRIDE", 5: "PRECOG_ERR_ALIGN", 6: "PRECOG_ERR_WORKSPACE",
           7: "PRECOG_ERR_ARCH", 8: "PRECOG_ERR_HIP"}
 
-EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode",
+EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_trajectory",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
            "precog_retrieve_topk", "precog_inject_gather", "precog_inject_compose",
            "precog_status_string")
@@ -62,6 +62,9 @@ def lib():
         L.precog_scan_workspace_bytes.restype = sz
         L.precog_scan_encode.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + [sz, vp]
         L.precog_scan_encode.restype = ctypes.c_int
+        L.precog_scan_trajectory.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + \
+            [i64, vp, sz, vp]
+        L.precog_scan_trajectory.restype = ctypes.c_int
         L.precog_retrieve_workspace_bytes.argtypes = [i64, i64, i64]
         L.precog_retrieve_workspace_bytes.restype = sz
         L.precog_retrieve_top1.argtypes = [vp, vp, i64, i64, i64, vp, vp, sz, vp]
@@ -122,6 +125,16 @@ def scan_encode(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None
                                   _ptr(C), _ptr(z), _ptr(Dskip), _ptr(h0), _ptr(y), _ptr(hT),
                                   _ptr(workspace), int(workspace_bytes), _stream(stream))
     _check("precog_scan_encode", st)
+
+
+def scan_trajectory(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None, y=None,
+                    hT=None, traj=None, every=1, workspace=None, workspace_bytes=0, stream=None):
+    """precog_scan_trajectory on device tensors (or raw device pointers)."""
+    st = lib().precog_scan_trajectory(ctypes.byref(desc), _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
+                                      _ptr(C), _ptr(z), _ptr(Dskip), _ptr(h0), _ptr(y), _ptr(hT),
+                                      _ptr(traj), int(every), _ptr(workspace),
+                                      int(workspace_bytes), _stream(stream))
+    _check("precog_scan_trajectory", st)
 
 
 def retrieve_workspace_bytes(Q, M, E) -> int:
@@ -185,6 +198,24 @@ def scan(x, dt, A, B, C=None, z=None, Dskip=None, h0=None, *, out_dtype=torch.fl
     scan_encode(desc, x, dt, A, B, C, z, Dskip, h0, y, hT if want_hT else None, ws, nbytes,
                 stream)
     return y, (hT if want_hT else None)
+
+
+def trajectory(x, dt, A, B, every, C=None, z=None, Dskip=None, h0=None, *,
+               out_dtype=torch.float32, state_dtype=torch.float32, want_y=False, want_hT=False,
+               chunk=0, stream=None):
+    """Runs the scan keeping every `every`-th state; returns (traj, y, hT)."""
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[state_dtype], 0, 0, chunk)
+    # every < 1 is left to the library to reject
+    traj = torch.empty((Bt, L // every if every >= 1 else 0, D, N), dtype=state_dtype,
+                       device=x.device)
+    y = torch.empty((Bt, L, D), dtype=out_dtype, device=x.device) if want_y else None
+    hT = torch.empty((Bt, D, N), dtype=state_dtype, device=x.device) if want_hT else None
+    nbytes = scan_workspace_bytes(desc)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    scan_trajectory(desc, x, dt, A, B, C, z, Dskip, h0, y, hT, traj, every, ws, nbytes, stream)
+    return traj, y, hT
 
 
 def top1(query, index, stream=None):

@@ -49,7 +49,8 @@ class ScanWorkload:
 
 # The five workloads: a single fp32 layer, corpus-chunk encoding, the query
 # prefill of query-time injection, a long-context scan and a large corpus
-# encode (per layer; 24 layers use seeds 5000 + layer).
+# encode (per layer; 24 layers use seeds 5000 + layer); then the SMC
+# trajectory encode.
 SINGLE_LAYER = ScanWorkload("single_layer_b1_l512_d128_n16_f32", 1, 512, 128, 16,
                             torch.float32, seed=1)
 CORPUS_ENCODE = ScanWorkload("corpus_encode_b64_l3000_d2048_n16_bf16", 64, 3000,
@@ -62,6 +63,11 @@ LARGE_CORPUS = ScanWorkload("large_corpus_b1024_l3000_d1536_n64_bf16_per_layer",
                             1024, 3000, 1536, 64, dt_mu=-3.0, dt_sigma=1.0,
                             seed=5000)
 LARGE_CORPUS_LAYERS = 24
+# SMC trajectory encode: 512-token conversation chunks (the paper's N_c), one
+# layer, captured at the fidelity dial's every = 1 (K = N_c), 8 and 512 (K = 1).
+SMC_TRAJECTORY = ScanWorkload("smc_trajectory_b64_l512_d2048_n16_bf16", 64, 512,
+                              2048, 16, seed=6)
+SMC_DIALS = (1, 8, 512)
 
 RETRIEVAL = dict(Q=256, M=10000, E=384, planted=32, seed=3)
 STATE_STORE = dict(M=10000, D=1024, N=16)

@@ -115,6 +115,25 @@ def test_retrieve_validation_errors():
     assert call(Q=0) == OK
 
 
+def test_trajectory_validation_errors():
+    L = P.lib()
+    good = P.scan_desc(2, 16, 64, 16)
+
+    def call(desc=good, traj=FAKE, every=4, x=FAKE):
+        return L.precog_scan_trajectory(ctypes.byref(desc), x, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                        None, FAKE, FAKE, traj, every, None, 0, None)
+    assert call(every=0) == ESHAPE
+    assert call(every=-3) == ESHAPE
+    assert call(traj=None) == ENULL
+    assert call(traj=FAKE + 4) == EALIGN
+    assert call(x=None) == ENULL
+    assert call(P.scan_desc(2, 16, 60, 16)) == EALIGN
+    assert call(P.scan_desc(0, 16, 64, 16)) == OK      # empty batch
+    # nothing to capture (L < every) and no other output: NULL traj is fine
+    assert L.precog_scan_trajectory(ctypes.byref(good), FAKE, FAKE, FAKE, FAKE, None, None, None,
+                                    None, None, None, None, 17, None, 0, None) == OK
+
+
 def test_topk_validation_errors():
     L = P.lib()
     ws = P.retrieve_workspace_bytes(4, 10, 16)
