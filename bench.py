@@ -289,6 +289,37 @@ def bench_extra(args):
     del inp, ws
     torch.cuda.empty_cache()
 
+    # SMC consolidation: route 64 chunks, fold their final states into the
+    # 20 semantic states (24 x 4096, fp16), then a session start (route the
+    # opening chunk, inject its semantic state)
+    cfg = synth.SMC
+    emb, dom, sub, _, _ = synth.smc_inputs_host(cfg["C"], cfg["E"], cfg["ndom"], cfg["nsub"],
+                                                cfg["seed"])
+    emb, dom, sub = emb.cuda(), dom.cuda(), sub.cuda()
+    R, S = cfg["ndom"] * cfg["nsub"], cfg["S"]
+    states = torch.zeros((R, S), dtype=torch.float16, device="cuda")
+    contrib = synth.state_store(cfg["C"], S, seed=34, device="cuda")
+    outs = [torch.empty(cfg["C"], dtype=torch.int32, device="cuda") for _ in range(3)]
+    one = [torch.empty(1, dtype=torch.int32, device="cuda") for _ in range(3)]
+    h_init = torch.empty((1, S), dtype=torch.float16, device="cuda")
+    ro_ms = time_events(lambda: P.smc_route(emb, dom, sub, *outs), 20)
+    co_ms = time_events(lambda: P.smc_consolidate(states, contrib, outs[2], 0.2), 20)
+
+    def session():
+        P.smc_route(emb[:1], dom, sub, *one)
+        P.inject_gather(states, one[2], h_init)
+
+    se_ms = time_events(session, 20)
+    res["smc"] = {
+        "workload": "64 chunks routed over 5 domains x 4 sub-clusters (E=384); semantic states "
+                    "[20, 24 x 4096] fp16, alpha = 0.2",
+        "route_ms": ro_ms, "consolidate_ms": co_ms,
+        "consolidate_gbps": (2 * R * S * 2 + cfg["C"] * S * 2) / (co_ms * 1e-3) / 1e9,
+        "session_start_ms": se_ms,
+    }
+    del states, contrib
+    torch.cuda.empty_cache()
+
     # long-context chunked scan (one timed call)
     wl = synth.LONG_CONTEXT
     B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate

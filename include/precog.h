@@ -14,10 +14,13 @@
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
  * with the SMC trajectory variant of the scan:
  *   precog_scan_trajectory  the scan keeping every k-th state (Sec. 5.1-5.2)
- * and the top-k extension of retrieval and injection:
+ * the top-k extension of retrieval and injection:
  *   precog_retrieve_topk    exact top-k with scores (Sec. 4.4, Fig. 1)
  *   precog_inject_compose   softmax-weighted composition of the top-k states
  *                           (Sec. 5.4 Eq. smc-fusion)
+ * and the memory-consolidation steps of SMC:
+ *   precog_smc_route        two-stage cluster routing (Sec. 5.1)
+ *   precog_smc_consolidate  semantic-state EMA (Sec. 5.3 Eq. smc-ema)
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are device pointers owned by the caller.  The
@@ -229,6 +232,48 @@ precog_status precog_inject_compose(const void *state_store,
                                     const double *score, int64_t Q, int64_t k,
                                     double tau, void *h0, precog_dtype h0_dtype,
                                     void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Structured Memory Consolidation (Sec. 5)                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Two-stage routing of Sec. 5.1 (Eqs. smc-domain, smc-sub) for C chunk
+ * embeddings phi(c):
+ *   domain_out[c] = m* = argmax_m <phi(c), p_m>
+ *   sub_out[c]    = j* = argmax_j <phi(c), q_{m*, j}>
+ *   flat_out[c]   = m* * n_sub + j* (the row of the sub-cluster's semantic
+ *                   state in an [n_domains * n_sub, S] table; NULL = skip)
+ * Scores are exact: fp64 sums of the exact products, in feature order;
+ * equal scores go to the lower index.  Non-finite inputs give unspecified
+ * (in-range) routes.
+ *   emb          [C, E] fp32     domain_protos [n_domains, E] fp32
+ *   sub_protos   [n_domains, n_sub, E] fp32
+ *   1 <= n_domains, n_sub <= 64; E % 4 == 0, 4 <= E <= 4096; outputs int32
+ *   [C]; pointers 16-byte aligned. */
+precog_status precog_smc_route(const float *emb, int64_t C, int64_t E,
+                               const float *domain_protos, int64_t n_domains,
+                               const float *sub_protos, int64_t n_sub,
+                               int32_t *domain_out, int32_t *sub_out,
+                               int32_t *flat_out, void *stream);
+
+/* Semantic consolidation of Sec. 5.3 (Eq. smc-ema), applied in chunk order:
+ *   for c = 0..C-1:  states[target[c]] <- (1 - alpha) states[target[c]]
+ *                                         + alpha contrib[c]
+ * in place, e.g. with target = flat_out of precog_smc_route and contrib =
+ * the chunks' final states (their K = 1 contributions).  A target outside
+ * [0, R) leaves every state unchanged for that chunk.  Each update is one
+ * fp32 fused multiply-add with alpha and 1 - alpha rounded once to fp32
+ * (alpha = 1 replaces the state exactly); F16 states are rounded to nearest
+ * even after every update, as separate calls would.
+ *   states   [R, S] F32 | F16, updated in place (R <= 65535)
+ *   contrib  [C, S] F32 | F16; must not overlap states
+ *   target   [C] int32
+ *   0 < alpha <= 1; S % 8 == 0; pointers 16-byte aligned */
+precog_status precog_smc_consolidate(void *states, precog_dtype state_dtype,
+                                     int64_t R, int64_t S, const void *contrib,
+                                     precog_dtype contrib_dtype,
+                                     const int32_t *target, int64_t C,
+                                     double alpha, void *stream);
 
 /* Static, human-readable name of a status code. */
 const char *precog_status_string(precog_status s);

@@ -17,8 +17,9 @@ What each function follows in the paper (arXiv 2608.02560):
   (Sec. 5.2).
 * ``topk_compose``-- softmax-weighted composition of the top-k states
   (Sec. 5.4, Eq. smc-fusion; Fig. 1 caption).
-* ``route2``, ``ema`` -- SMC two-stage routing (Sec. 5.1, Eqs. smc-domain,
-  smc-sub) and semantic EMA consolidation (Sec. 5.3, Eq. smc-ema).
+* ``route2``, ``ema``, ``consolidate`` -- SMC two-stage routing (Sec. 5.1,
+  Eqs. smc-domain, smc-sub) and semantic EMA consolidation (Sec. 5.3,
+  Eq. smc-ema), one update and a chunk-ordered sequence of them.
 * ``round_bf16``, ``round_f16`` -- round-to-nearest-even storage rounding of
   fp64 values (the paper stores states at FP16, Sec. 4.2).
 """
@@ -217,6 +218,18 @@ def route2(emb, domain_protos, sub_protos):
 def ema(state, contribution, alpha):
     """Semantic consolidation s <- (1 - alpha) s + alpha h (Sec. 5.3, Eq. smc-ema)."""
     return (1.0 - alpha) * _f64(state) + alpha * _f64(contribution)
+
+
+def consolidate(states, contrib, target, alpha):
+    """Eq. smc-ema applied for every chunk in chunk order (Sec. 5.3): chunk c
+    updates the semantic state of its sub-cluster target[c]; targets outside
+    the table leave it unchanged.  fp64."""
+    out = _f64(states).copy()
+    h = _f64(contrib)
+    for c, r in enumerate(np.asarray(target, dtype=np.int64)):
+        if 0 <= r < out.shape[0]:
+            out[r] = ema(out[r], h[c], alpha)
+    return out
 
 
 def round_bf16(a):

@@ -406,4 +406,68 @@ precog_status precog_inject_compose(const void* state_store, precog_dtype store_
   return PRECOG_OK;
 }
 
+precog_status precog_smc_route(const float* emb, int64_t C, int64_t E, const float* domain_protos,
+                              int64_t n_domains, const float* sub_protos, int64_t n_sub,
+                              int32_t* domain_out, int32_t* sub_out, int32_t* flat_out,
+                              void* stream) {
+  if (C < 0 || E < 4 || E > 4096 || n_domains < 1 || n_domains > 64 || n_sub < 1 || n_sub > 64)
+    return PRECOG_ERR_SHAPE;
+  if (E % 4 != 0) return PRECOG_ERR_ALIGN;
+  if (C > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (C == 0) return PRECOG_OK;
+  if (!emb || !domain_protos || !sub_protos || !domain_out || !sub_out) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {emb, domain_protos, sub_protos, domain_out, sub_out, flat_out};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+  precog::RouteParams p{};
+  p.emb = emb;
+  p.dom = domain_protos;
+  p.sub = sub_protos;
+  p.dom_out = domain_out;
+  p.sub_out = sub_out;
+  p.flat_out = flat_out;
+  p.C = C;
+  p.E = E;
+  p.ndom = static_cast<int>(n_domains);
+  p.nsub = static_cast<int>(n_sub);
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_route(p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
+precog_status precog_smc_consolidate(void* states, precog_dtype state_dtype, int64_t R, int64_t S,
+                                     const void* contrib, precog_dtype contrib_dtype,
+                                     const int32_t* target, int64_t C, double alpha,
+                                     void* stream) {
+  if (R < 0 || S < 0 || C < 0) return PRECOG_ERR_SHAPE;
+  if (!(alpha > 0.0 && alpha <= 1.0)) return PRECOG_ERR_SHAPE;
+  if ((state_dtype != PRECOG_F32 && state_dtype != PRECOG_F16) ||
+      (contrib_dtype != PRECOG_F32 && contrib_dtype != PRECOG_F16))
+    return PRECOG_ERR_DTYPE;
+  if (S % 8 != 0) return PRECOG_ERR_ALIGN;
+  if (R == 0 || S == 0 || C == 0) return PRECOG_OK;
+  if (R > 65535 || S / 8 / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (!states || !contrib || !target) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {states, contrib, target};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return PRECOG_ERR_ALIGN;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+  precog::EmaParams p{};
+  p.states = states;
+  p.contrib = contrib;
+  p.target = target;
+  p.R = R;
+  p.S = S;
+  p.C = C;
+  p.alpha = static_cast<float>(alpha);
+  p.one_minus_alpha = static_cast<float>(1.0 - alpha);
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_ema(p, state_dtype, contrib_dtype,
+                                          static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
 }  // extern "C"

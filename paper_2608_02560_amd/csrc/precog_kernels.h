@@ -91,6 +91,27 @@ struct ComposeParams {
 hipError_t launch_compose(const ComposeParams& p, int store_dtype, int out_dtype,
                           hipStream_t s);
 
+struct RouteParams {
+  const float* emb;    // [C, E] chunk embeddings
+  const float* dom;    // [ndom, E] domain prototypes
+  const float* sub;    // [ndom, nsub, E] sub-cluster prototypes
+  int32_t* dom_out;    // [C]
+  int32_t* sub_out;    // [C]
+  int32_t* flat_out;   // [C] dom * nsub + sub, or null
+  int64_t C, E;
+  int ndom, nsub;      // 1..64 each
+};
+hipError_t launch_route(const RouteParams& p, hipStream_t s);
+
+struct EmaParams {
+  void* states;          // [R, S] semantic states, updated in place
+  const void* contrib;   // [C, S] chunk contributions
+  const int32_t* target; // [C] row of states per chunk; outside [0, R): none
+  int64_t R, S, C;
+  float alpha, one_minus_alpha;
+};
+hipError_t launch_ema(const EmaParams& p, int state_dtype, int contrib_dtype, hipStream_t s);
+
 // Raw buffer descriptor over [base, base + bytes): loads at or past `bytes`
 // return zero and stores there are dropped by the hardware range check.
 constexpr int kBufWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)

@@ -1,0 +1,159 @@
+// Structured Memory Consolidation on gfx950 (Sec. 5): two-stage cluster
+// routing (Sec. 5.1, Eqs. smc-domain and smc-sub) and the semantic EMA
+// (Sec. 5.3, Eq. smc-ema).
+//
+// Routing is exact: every score is the fp64 sum of the exact products of two
+// fp32 values, summed in feature order (one fused multiply-add per term,
+// which rounds exactly as multiply-then-add here), and the argmax keeps the
+// lowest index among equal scores.  One wave per chunk embedding; lane m
+// scores prototype m sequentially.  The work is a few thousand fused
+// multiply-adds per chunk, so the kernel is latency-bound by design.
+//
+// Consolidation applies s <- (1 - alpha) s + alpha h to the routed semantic
+// state for every chunk in chunk order; rows and element slices run in
+// parallel, the chunks of one row in order within one lane.
+#include <type_traits>
+
+#include "precog_kernels.h"
+
+namespace precog {
+namespace {
+
+constexpr int kMaxE = 4096;
+
+__device__ __forceinline__ double shfl_d(double v, int src_lane) {
+  const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2loint(v)));
+  const int hi = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2hiint(v)));
+  return __hiloint2double(hi, lo);
+}
+
+// fp64 dot product of the embedding in LDS with one prototype row, in
+// feature order.
+__device__ __forceinline__ double exact_dot(const float4* e4, const float* row, int E) {
+  const float4* r4 = reinterpret_cast<const float4*>(row);
+  double s = 0.0;
+  for (int i = 0; i < E / 4; ++i) {
+    const float4 a = e4[i];
+    const float4 b = r4[i];
+    s = fma(static_cast<double>(a.x), static_cast<double>(b.x), s);
+    s = fma(static_cast<double>(a.y), static_cast<double>(b.y), s);
+    s = fma(static_cast<double>(a.z), static_cast<double>(b.z), s);
+    s = fma(static_cast<double>(a.w), static_cast<double>(b.w), s);
+  }
+  return s;
+}
+
+// Lane holding the best (score, lowest index) among lanes < n.
+__device__ __forceinline__ int wave_argmax(double s, int lane, int n) {
+  double bs = lane < n ? s : -INFINITY;
+  int bi = lane < n ? lane : 0x7fffffff;
+  bool any = lane < n;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    const double os = shfl_d(bs, lane ^ m);
+    const int oi = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, bi);
+    const bool oany = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(any)) != 0;
+    if (oany && (!any || os > bs || (os == bs && oi < bi))) {
+      bs = os;
+      bi = oi;
+      any = true;
+    }
+  }
+  return bi;
+}
+
+__global__ __launch_bounds__(64) void route_kernel(const RouteParams p) {
+  const int64_t c = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int E = static_cast<int>(p.E);
+  __shared__ float4 e4[kMaxE / 4];
+  const float4* src = reinterpret_cast<const float4*>(p.emb + c * p.E);
+  for (int i = lane; i < E / 4; i += 64) e4[i] = src[i];
+  __syncthreads();
+  // stage 1: domain m* = argmax_m <phi(c), p_m>
+  double s = 0.0;
+  if (lane < p.ndom) s = exact_dot(e4, p.dom + static_cast<int64_t>(lane) * p.E, E);
+  const int m = wave_argmax(s, lane, p.ndom);
+  // stage 2: sub-cluster j* = argmax_j <phi(c), q_{m*, j}>
+  s = 0.0;
+  if (lane < p.nsub) s = exact_dot(e4, p.sub + (static_cast<int64_t>(m) * p.nsub + lane) * p.E, E);
+  const int j = wave_argmax(s, lane, p.nsub);
+  if (lane == 0) {
+    p.dom_out[c] = m;
+    p.sub_out[c] = j;
+    if (p.flat_out) p.flat_out[c] = m * p.nsub + j;
+  }
+}
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float8 __attribute__((ext_vector_type(8)));
+
+template <typename T> struct V8;
+template <> struct V8<float> {
+  static __device__ __forceinline__ float8 load(const void* b, int64_t i) {
+    return *reinterpret_cast<const float8*>(static_cast<const float*>(b) + i);
+  }
+  static __device__ __forceinline__ void store(void* b, int64_t i, float8 v) {
+    *reinterpret_cast<float8*>(static_cast<float*>(b) + i) = v;
+  }
+};
+template <> struct V8<f16_t> {
+  static __device__ __forceinline__ float8 load(const void* b, int64_t i) {
+    return __builtin_convertvector(*reinterpret_cast<const half8*>(static_cast<const _Float16*>(b) + i),
+                                   float8);
+  }
+  static __device__ __forceinline__ void store(void* b, int64_t i, float8 v) {
+    *reinterpret_cast<half8*>(static_cast<_Float16*>(b) + i) = __builtin_convertvector(v, half8);
+  }
+};
+
+// Workgroup (slice, r): state row r, elements [2048 slice, 2048 slice + 2048).
+// The row slice is loaded once, every chunk routed to r is applied in chunk
+// order in registers, and the slice is stored once, so states are read and
+// written once and each contribution is read once.  Each update is
+// s' = fma(alpha, h, (1 - alpha) s) in fp32 with both factors rounded once
+// from fp64 (alpha = 1 gives s' = h exactly); fp16 states are rounded to
+// nearest even after every update, as an fp16 store would be.
+template <typename TS, typename TH>
+__global__ __launch_bounds__(256) void ema_kernel(const EmaParams p) {
+  const int64_t r = blockIdx.y;
+  const int64_t e = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (e >= p.S) return;
+  const float a = p.alpha;
+  const float b = p.one_minus_alpha;
+  const int64_t so = r * p.S + e;
+  float8 s = V8<TS>::load(p.states, so);
+  bool touched = false;
+  for (int64_t c = 0; c < p.C; ++c) {
+    if (p.target[c] != r) continue;  // wave-uniform: same chunk list for all lanes
+    const float8 h = V8<TH>::load(p.contrib, c * p.S + e);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s[k] = fmaf(a, h[k], b * s[k]);
+    if constexpr (std::is_same<TS, f16_t>::value)
+      s = __builtin_convertvector(__builtin_convertvector(s, half8), float8);
+    touched = true;
+  }
+  if (touched) V8<TS>::store(p.states, so, s);
+}
+
+}  // namespace
+
+hipError_t launch_route(const RouteParams& p, hipStream_t s) {
+  hipLaunchKernelGGL(route_kernel, dim3(static_cast<unsigned>(p.C)), dim3(64), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_ema(const EmaParams& p, int state_dtype, int contrib_dtype, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>((p.S / 8 + 255) / 256), static_cast<unsigned>(p.R));
+  if (state_dtype == 0 && contrib_dtype == 0)
+    hipLaunchKernelGGL((ema_kernel<float, float>), grid, dim3(256), 0, s, p);
+  else if (state_dtype == 0)
+    hipLaunchKernelGGL((ema_kernel<float, f16_t>), grid, dim3(256), 0, s, p);
+  else if (contrib_dtype == 0)
+    hipLaunchKernelGGL((ema_kernel<f16_t, float>), grid, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((ema_kernel<f16_t, f16_t>), grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace precog

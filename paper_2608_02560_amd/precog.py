@@ -27,7 +27,7 @@ STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECO
 EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_trajectory",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
            "precog_retrieve_topk", "precog_inject_gather", "precog_inject_compose",
-           "precog_status_string")
+           "precog_smc_route", "precog_smc_consolidate", "precog_status_string")
 
 
 class PrecogError(RuntimeError):
@@ -77,6 +77,11 @@ def lib():
         L.precog_inject_compose.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, i64,
                                             ctypes.c_double, vp, ctypes.c_int, vp]
         L.precog_inject_compose.restype = ctypes.c_int
+        L.precog_smc_route.argtypes = [vp, i64, i64, vp, i64, vp, i64, vp, vp, vp, vp]
+        L.precog_smc_route.restype = ctypes.c_int
+        L.precog_smc_consolidate.argtypes = [vp, ctypes.c_int, i64, i64, vp, ctypes.c_int, vp, i64,
+                                             ctypes.c_double, vp]
+        L.precog_smc_consolidate.restype = ctypes.c_int
         L.precog_status_string.argtypes = [ctypes.c_int]
         L.precog_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -179,6 +184,24 @@ def inject_gather(store, idx, h0, stream=None):
     _check("precog_inject_gather", st)
 
 
+def smc_route(emb, domain_protos, sub_protos, domain_out, sub_out, flat_out=None, stream=None):
+    C, E = emb.shape
+    st = lib().precog_smc_route(_ptr(emb), C, E, _ptr(domain_protos), domain_protos.shape[0],
+                                _ptr(sub_protos), sub_protos.shape[1], _ptr(domain_out),
+                                _ptr(sub_out), _ptr(flat_out), _stream(stream))
+    _check("precog_smc_route", st)
+
+
+def smc_consolidate(states, contrib, target, alpha, stream=None):
+    R = states.shape[0]
+    S = states[0].numel() if R > 0 else 0
+    C = target.shape[0]
+    st = lib().precog_smc_consolidate(_ptr(states), _DT[states.dtype], R, S, _ptr(contrib),
+                                      _DT[contrib.dtype], _ptr(target), C, float(alpha),
+                                      _stream(stream))
+    _check("precog_smc_consolidate", st)
+
+
 # ----------------------------------------------------------------------------
 # Convenience wrappers that allocate outputs and workspace with torch.
 # ----------------------------------------------------------------------------
@@ -246,6 +269,14 @@ def compose(store, idx, score, tau=1.0, out_dtype=None, stream=None):
                      device=store.device)
     inject_compose(store, idx, score, tau, h0, stream)
     return h0
+
+
+def route(emb, domain_protos, sub_protos, stream=None):
+    """Two-stage routing: returns (domain int32 [C], sub int32 [C], flat int32 [C])."""
+    C = emb.shape[0]
+    outs = [torch.empty(C, dtype=torch.int32, device=emb.device) for _ in range(3)]
+    smc_route(emb, domain_protos, sub_protos, *outs, stream=stream)
+    return tuple(outs)
 
 
 def gather(store, idx, out_dtype=None, stream=None):

@@ -162,6 +162,33 @@ def retrieval_inputs_host(Q: int, M: int, E: int, planted: int, seed: int):
             torch.from_numpy(pos), torch.from_numpy(rows))
 
 
+# SMC memory: M = 5 cognitive domains x J = 4 sub-clusters with 384-dim
+# prototypes, semantic states of 24 layers x 4096 (192 KB at fp16, Sec. 5.3),
+# 64 chunks deposited per consolidation call.
+SMC = dict(C=64, E=384, ndom=5, nsub=4, S=24 * 4096, seed=7)
+
+
+def smc_inputs_host(C: int, E: int, ndom: int, nsub: int, seed: int, spread: float = 0.3):
+    """Unit-norm domain prototypes p_m, sub-cluster prototypes q_{m,j} =
+    normalize(p_m + spread * noise), and chunk embeddings planted near a
+    drawn sub-cluster: phi(c) = normalize(q_{m,j} + 0.05 * noise).  Returns
+    (emb [C, E], dom [ndom, E], sub [ndom, nsub, E], planted_m [C],
+    planted_j [C]); the plants make the expected routes known independently
+    of any scoring code."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    dom = unit_rows_host(ndom, E, g).astype(np.float64)
+    sub = np.empty((ndom, nsub, E))
+    for m in range(ndom):
+        v = dom[m] + spread * g.standard_normal((nsub, E)) / np.sqrt(E)
+        sub[m] = v / np.linalg.norm(v, axis=1, keepdims=True)
+    pm = g.integers(0, ndom, C)
+    pj = g.integers(0, nsub, C)
+    v = sub[pm, pj] + 0.05 * g.standard_normal((C, E)) / np.sqrt(E)
+    emb = v / np.linalg.norm(v, axis=1, keepdims=True)
+    f = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return f(emb), f(dom), f(sub), torch.from_numpy(pm), torch.from_numpy(pj)
+
+
 def state_store(M: int, S: int, seed: int, device: str = "cpu",
                 dtype: torch.dtype = torch.float16):
     """A store of M precomputed states of S elements each, N(0, 1)."""

@@ -168,6 +168,32 @@ def test_compose_validation_errors():
     assert call(Q=0) == OK
 
 
+def test_smc_validation_errors():
+    L = P.lib()
+    route = lambda e=FAKE, C=3, E=16, d=FAKE, nd=5, s=FAKE, ns=4, mo=FAKE, so=FAKE, fo=None: \
+        L.precog_smc_route(e, C, E, d, nd, s, ns, mo, so, fo, None)
+    assert route(nd=0) == ESHAPE
+    assert route(ns=65) == ESHAPE
+    assert route(E=2) == ESHAPE
+    assert route(E=18) == EALIGN
+    assert route(d=None) == ENULL
+    assert route(so=None) == ENULL
+    assert route(fo=FAKE + 4) == EALIGN
+    assert route(C=0) == OK
+    cons = lambda st=FAKE, sd=P.F16, R=20, S=64, h=FAKE, hd=P.F16, t=FAKE, C=3, a=0.25: \
+        L.precog_smc_consolidate(st, sd, R, S, h, hd, t, C, a, None)
+    assert cons(a=0.0) == ESHAPE
+    assert cons(a=1.5) == ESHAPE
+    assert cons(a=float("nan")) == ESHAPE
+    assert cons(R=70000) == ESHAPE
+    assert cons(sd=P.BF16) == EDTYPE
+    assert cons(S=12) == EALIGN
+    assert cons(t=None) == ENULL
+    assert cons(h=FAKE + 2) == EALIGN
+    assert cons(C=0) == OK
+    assert cons(a=1.0, C=0) == OK
+
+
 def test_gather_validation_errors():
     L = P.lib()
     call = lambda s=FAKE, sd=P.F16, M=10, S=64, idx=FAKE, Q=3, h=FAKE, hd=P.F32: \

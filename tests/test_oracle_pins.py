@@ -401,3 +401,28 @@ def test_ema_fixed_point_and_alpha_one():
     for _ in range(200):
         cur = oracle.ema(cur, h, 0.25)
     assert np.allclose(cur, h, atol=1e-20 + 1e-12)
+
+
+def test_consolidate_closed_form_and_skips():
+    """Repeated deposits into one sub-cluster follow the unrolled EMA,
+    s_n = (1-a)^n s_0 + sum_k a (1-a)^(n-1-k) h_k; other rows and
+    out-of-table targets change nothing."""
+    g = np.random.default_rng(11)
+    states = g.normal(size=(4, 6))
+    contrib = g.normal(size=(5, 6))
+    target = np.array([2, -1, 2, 4, 2])
+    a = 0.3
+    out = oracle.consolidate(states, contrib, target, a)
+    hs = contrib[[0, 2, 4]]
+    ref = (1 - a) ** 3 * states[2] + sum(a * (1 - a) ** (2 - k) * hs[k] for k in range(3))
+    assert np.allclose(out[2], ref, rtol=0, atol=1e-14)
+    for r in (0, 1, 3):
+        assert np.array_equal(out[r], states[r])
+
+
+def test_smc_planted_routes():
+    """Chunks planted next to sub-cluster prototypes route to them (Eqs.
+    smc-domain and smc-sub), a check that does not use the oracle's scores."""
+    emb, dom, sub, pm, pj = synth.smc_inputs_host(64, 384, 5, 4, seed=7)
+    m, j = oracle.route2(emb, dom, sub)
+    assert np.array_equal(m, pm.numpy()) and np.array_equal(j, pj.numpy())
