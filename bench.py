@@ -34,7 +34,7 @@ HBM_PEAK_GBPS = 8000.0
 VALU_PEAK_TFLOPS = 157.3
 SLOT_FLOPS_PER_TDN = 16
 PROFILE = os.path.join(ROOT, "profiles", "scan_corpus_encode_b64_l3000_d2048_n16.md")
-SCAN_SOURCE = os.path.join(ROOT, "paper_2608_02560_amd", "csrc", "scan.hip")
+SCAN_SOURCE = os.path.join(ROOT, "paper_2608_02560_amd", "csrc", "scan_kernels.h")
 
 
 def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate=True):
@@ -67,7 +67,7 @@ def measured_traffic():
         if ":" in line and line.strip().startswith("- "):
             k, v = line.strip()[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    if fields.get("scan.hip sha256") != src:
+    if fields.get("scan_kernels.h sha256") != src:
         return None
     try:
         return float(fields["traffic bytes per launch"])
