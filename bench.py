@@ -320,6 +320,26 @@ def bench_extra(args):
     del states, contrib
     torch.cuda.empty_cache()
 
+    # complex-A scan on the corpus-encode shape (w_n = pi n)
+    wl = synth.COMPLEX_ENCODE
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
+    A_im = synth.complex_frequencies(D, N).cuda()
+    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((B, D, N, 2), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16)
+    run = lambda: P.scan_complex_raw(desc, inp["x"], inp["dt"], inp["A"], A_im, inp["B"],
+                                     inp["C"], inp["z"], inp["Dskip"], None, y, hT)
+    run()
+    x_ms = time_events(run, 5)
+    nb = scan_bytes(B, L, D, N) + B * D * N * 2  # hT has two parts
+    res["complex_encode"] = {"workload": wl.name + ", w_n = pi n, fp16 complex hT",
+                             "ms": x_ms, "tokens_per_s": B * L / (x_ms * 1e-3),
+                             "gbps": nb / (x_ms * 1e-3) / 1e9,
+                             "transcendentals_per_s": 3 * B * L * D * N / (x_ms * 1e-3)}
+    del inp, y, hT, A_im
+    torch.cuda.empty_cache()
+
     # long-context chunked scan (one timed call)
     wl = synth.LONG_CONTEXT
     B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate

@@ -12,8 +12,9 @@
  *                           captured hT (Eq. 1, Sec. 3; capture, Sec. 4.2)
  *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
- * with the SMC trajectory variant of the scan:
+ * with the SMC trajectory variant of the scan and the complex-A scan:
  *   precog_scan_trajectory  the scan keeping every k-th state (Sec. 5.1-5.2)
+ *   precog_scan_complex     Eq. 1 with a diagonal complex A (Sec. 3)
  * the top-k extension of retrieval and injection:
  *   precog_retrieve_topk    exact top-k with scores (Sec. 4.4, Fig. 1)
  *   precog_inject_compose   softmax-weighted composition of the top-k states
@@ -146,6 +147,29 @@ precog_status precog_scan_trajectory(const precog_scan_desc *desc,
                                      void *y, void *hT, void *traj,
                                      int64_t every, void *workspace,
                                      size_t workspace_bytes, void *stream);
+
+/* The scan with the diagonal complex A of Sec. 3 (Eq. 1 with A_k = a_k +
+ * i w_k; the paper's frequencies are w_k = pi k, its real part is the
+ * negative of a here, see precog_scan_encode):
+ *
+ *   h_t[d,n] = exp(-dt_t[d] (A_re[d,n] + i A_im[d,n])) h_{t-1}[d,n]
+ *              + B_t[n] x_t[d] dt_t[d]                       (complex state)
+ *   y_t[d]   = (sum_n C_t[n] Re h_t[d,n] + Dskip[d] x_t[d]) * silu(z_t[d])
+ *
+ * Arguments as precog_scan_encode, except:
+ *   A_re, A_im  [D, N] fp32; A_re > 0.
+ *   h0, hT      complex state rows [D, N, 2] ((real, imaginary) interleaved)
+ *               in desc->state_dtype; batch strides in elements, 0 = 2*D*N.
+ *   desc->dstate in {1, 2, 4, 8, 16}; one pass over the sequence
+ *               (desc->chunk 0 or >= L), so no workspace.
+ * The rotation uses the hardware sine and cosine of the angle reduced to
+ * [0, 1) revolutions; the magnitude uses the hardware exp2. */
+precog_status precog_scan_complex(const precog_scan_desc *desc, const void *x,
+                                  const void *dt, const float *A_re,
+                                  const float *A_im, const void *B,
+                                  const void *C, const void *z,
+                                  const float *Dskip, const void *h0, void *y,
+                                  void *hT, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Cosine top-1 retrieval                                                   */

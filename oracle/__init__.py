@@ -13,6 +13,7 @@ What each function follows in the paper (arXiv 2608.02560):
   and the gated readout read as (C_t . h_t + Dskip x_t) * silu(z_t).
 * ``top1``        -- cosine top-1 over unit-norm keys (Sec. 4.2, query time).
 * ``gather``      -- state injection h_init <- h^(i*) (Sec. 4.2, query time).
+* ``scan_complex`` -- Eq. 1 with the diagonal complex A of Sec. 3.
 * ``trajectory``  -- SMC per-step trajectory (Sec. 5.1) thinned by the dial K
   (Sec. 5.2).
 * ``topk_compose``-- softmax-weighted composition of the top-k states
@@ -61,6 +62,8 @@ def _load():
         lib.oracle_scan_f64.restype = ctypes.c_int
         lib.oracle_trajectory_f64.argtypes = [i64] * 5 + [dp] * 6
         lib.oracle_trajectory_f64.restype = ctypes.c_int
+        lib.oracle_scan_complex_f64.argtypes = [i64, i64, i64, i64] + [dp] * 11
+        lib.oracle_scan_complex_f64.restype = ctypes.c_int
         lib.oracle_top1_f64.argtypes = [i64, i64, i64, fp, fp, ip, dp, ctypes.c_int]
         lib.oracle_top1_f64.restype = ctypes.c_int
         _lib = lib
@@ -109,6 +112,25 @@ def scan(x, dt, A, B, C, z=None, Dskip=None, h0=None, want_y=True,
                                  _ptr(h0), _ptr(y), _ptr(hT), int(nthreads))
     if rc:
         raise RuntimeError("oracle_scan_f64 failed with code %d" % rc)
+    return y, hT
+
+
+def scan_complex(x, dt, A_re, A_im, B, C, z=None, Dskip=None, h0=None, want_y=True):
+    """Eq. 1 with the diagonal complex A of Sec. 3, A = A_re + i A_im
+    (A_re > 0): complex state, real input term B x dt, readout of the real
+    part of C . h (gated as in ``scan``).  h0 and the returned hT are
+    [Bt, D, N, 2] with (real, imaginary) interleaved.  Returns (y, hT)."""
+    x, dt, A_re, A_im, B, C, z, Dskip, h0 = (_f64(v) for v in (x, dt, A_re, A_im, B, C, z,
+                                                              Dskip, h0))
+    Bt, L, D = x.shape
+    N = A_re.shape[1]
+    y = np.zeros((Bt, L, D)) if want_y else None
+    hT = np.zeros((Bt, D, N, 2))
+    rc = _load().oracle_scan_complex_f64(Bt, L, D, N, _ptr(x), _ptr(dt), _ptr(A_re),
+                                         _ptr(A_im), _ptr(B), _ptr(C), _ptr(z), _ptr(Dskip),
+                                         _ptr(h0), _ptr(y), _ptr(hT))
+    if rc:
+        raise RuntimeError("oracle_scan_complex_f64 failed with code %d" % rc)
     return y, hT
 
 

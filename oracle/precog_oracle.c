@@ -20,11 +20,16 @@
  *   oracle_trajectory_f64  SMC per-step trajectory (Sec. 5.1, Eq. smc-trajectory)
  *                       thinned by the fidelity dial K (Sec. 5.2): every k-th
  *                       state h_k, h_2k, ... plus nothing else.
+ *   oracle_scan_complex_f64  Eq. 1 with the diagonal complex A of Sec. 3,
+ *                       A_k = a_k + i w_k (a_k > 0 in this sign convention):
+ *                       complex state, real input term, readout of the real
+ *                       part of C_t . h_t.
  *
  * Rows (b, d) of the scan are independent (the recurrence is diagonal in the
  * state, Eq. 1), so the driver may hand disjoint row ranges to threads; each
  * row is still computed strictly in time order.
  */
+#include <complex.h>
 #include <math.h>
 #include <pthread.h>
 #include <stdint.h>
@@ -142,6 +147,65 @@ int oracle_scan_f64(int64_t B, int64_t L, int64_t D, int64_t N,
     free(th);
     free(jobs);
     return rc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Complex diagonal A                                                         */
+/* ------------------------------------------------------------------------- */
+
+/* h_t[n] = exp(-dt_t (a[n] + i w[n])) h_{t-1}[n] + B_t[n] x_t dt_t   (complex)
+ * y_t    = (sum_n C_t[n] Re(h_t[n]) + Dskip x_t) * silu(z_t)
+ * h0, hT : [B, D, N, 2] with (real, imaginary) interleaved; h0 NULL = 0.
+ * Arguments otherwise as oracle_scan_f64 (y and hT may be NULL). */
+int oracle_scan_complex_f64(int64_t B, int64_t L, int64_t D, int64_t N,
+                            const double *x, const double *dt, const double *Are,
+                            const double *Aim, const double *Bm, const double *Cm,
+                            const double *z, const double *Dskip, const double *h0,
+                            double *y, double *hT)
+{
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || !Are || !Aim)
+        return 1;
+    if (L > 0 && (!x || !dt || !Bm))
+        return 2;
+    if (y && L > 0 && !Cm)
+        return 3;
+    double complex *h = (double complex *)malloc((size_t)N * sizeof(double complex));
+    if (!h)
+        return 4;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t d = 0; d < D; ++d) {
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t o = ((b * D + d) * N + n) * 2;
+                h[n] = h0 ? h0[o] + I * h0[o + 1] : 0.0;
+            }
+            for (int64_t t = 0; t < L; ++t) {
+                const int64_t td = (b * L + t) * D + d;
+                const int64_t tn = (b * L + t) * N;
+                for (int64_t n = 0; n < N; ++n) {
+                    const double complex A = Are[d * N + n] + I * Aim[d * N + n];
+                    h[n] = cexp(-dt[td] * A) * h[n] + Bm[tn + n] * x[td] * dt[td];
+                }
+                if (y) {
+                    double acc = 0.0;
+                    for (int64_t n = 0; n < N; ++n)
+                        acc += Cm[tn + n] * creal(h[n]);
+                    double out = acc + (Dskip ? Dskip[d] * x[td] : 0.0);
+                    if (z) {
+                        const double zv = z[td];
+                        out *= zv / (1.0 + exp(-zv));
+                    }
+                    y[td] = out;
+                }
+            }
+            if (hT)
+                for (int64_t n = 0; n < N; ++n) {
+                    const int64_t o = ((b * D + d) * N + n) * 2;
+                    hT[o] = creal(h[n]);
+                    hT[o + 1] = cimag(h[n]);
+                }
+        }
+    free(h);
+    return 0;
 }
 
 /* ------------------------------------------------------------------------- */

@@ -470,4 +470,60 @@ precog_status precog_smc_consolidate(void* states, precog_dtype state_dtype, int
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 
+precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, const void* dt,
+                                  const float* A_re, const float* A_im, const void* B,
+                                  const void* C, const void* z, const float* Dskip,
+                                  const void* h0, void* y, void* hT, void* stream) {
+  precog_status st = validate_desc(desc);
+  if (st != PRECOG_OK) return st;
+  const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
+  if (N > 16) return PRECOG_ERR_SHAPE;
+  if (desc->chunk != 0 && desc->chunk < L) return PRECOG_ERR_SHAPE;  // one pass only
+  const int64_t dn2 = 2 * D * N;
+  if ((desc->h0_batch_stride != 0 && desc->h0_batch_stride < dn2) ||
+      (desc->hT_batch_stride != 0 && desc->hT_batch_stride < dn2))
+    return PRECOG_ERR_STRIDE;
+  if (Bt == 0 || D == 0) return PRECOG_OK;
+  const bool work = L > 0;
+  if (!A_re || !A_im) return PRECOG_ERR_NULL;
+  if (work && (!x || !dt || !B)) return PRECOG_ERR_NULL;
+  if (work && y && !C) return PRECOG_ERR_NULL;
+  if ((!y || !work) && !hT) return PRECOG_OK;  // nothing requested
+  const void* ptrs[] = {x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  const int64_t dblocks = ceil_div(D, kBlock);
+  if (dblocks * Bt > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  precog::ScanParams p{};
+  p.x = x;
+  p.dt = dt;
+  p.z = y ? z : nullptr;
+  p.Bm = B;
+  p.Cm = y ? C : nullptr;
+  p.A = A_re;
+  p.A_im = A_im;
+  p.Dskip = y ? Dskip : nullptr;
+  p.h0 = h0;
+  p.y = work ? y : nullptr;
+  p.hT = hT;
+  p.B = Bt;
+  p.L = L;
+  p.D = D;
+  p.chunk = L;
+  p.h0_stride = desc->h0_batch_stride ? desc->h0_batch_stride : dn2;
+  p.hT_stride = desc->hT_batch_stride ? desc->hT_batch_stride : dn2;
+  p.nchunks = 1;
+  p.dblocks = static_cast<int>(dblocks);
+  p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
+            (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_scan_complex(p, static_cast<int>(N), desc->in_dtype,
+                                                   desc->out_dtype, desc->state_dtype,
+                                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
 }  // extern "C"

@@ -26,6 +26,7 @@ struct ScanParams {
   const void* Bm;
   const void* Cm;
   const float* A;
+  const float* A_im;  // imaginary part of A (complex-A launches only)
   const float* Dskip;
   const void* h0;
   void* y;
@@ -48,6 +49,9 @@ hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
                        int state_dtype, hipStream_t s);
 hipError_t launch_scan_traj(const ScanParams& p, int N, int in_dtype, int out_dtype,
                             int state_dtype, hipStream_t s);
+// Complex diagonal A: one pass, N <= 16, states interleaved (re, im).
+hipError_t launch_scan_complex(const ScanParams& p, int N, int in_dtype, int out_dtype,
+                               int state_dtype, hipStream_t s);
 
 struct RetrieveParams {
   const float* q;      // [Q, E]

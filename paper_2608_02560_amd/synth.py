@@ -73,6 +73,17 @@ RETRIEVAL = dict(Q=256, M=10000, E=384, planted=32, seed=3)
 STATE_STORE = dict(M=10000, D=1024, N=16)
 
 
+# Complex-A variant: the corpus-encode shape with frequencies w_n = pi n
+# (Sec. 3), complex fp32 state.
+COMPLEX_ENCODE = ScanWorkload("complex_encode_b64_l3000_d2048_n16_bf16", 64, 3000,
+                              2048, 16, seed=8)
+
+
+def complex_frequencies(D: int, N: int) -> torch.Tensor:
+    """A_im[d, n] = pi n, the paper's imaginary part of A (Sec. 3), fp32."""
+    return torch.from_numpy(np.tile(np.pi * np.arange(N, dtype=np.float64), (D, 1))).float()
+
+
 def _softplus64(v: np.ndarray) -> np.ndarray:
     return np.logaddexp(0.0, v)
 

@@ -134,6 +134,22 @@ def test_trajectory_validation_errors():
                                     None, None, None, None, 17, None, 0, None) == OK
 
 
+def test_complex_scan_validation_errors():
+    L = P.lib()
+
+    def call(desc, x=FAKE, Aim=FAKE, h0=None):
+        return L.precog_scan_complex(ctypes.byref(desc), x, FAKE, FAKE, Aim, FAKE, FAKE, FAKE,
+                                     FAKE, h0, FAKE, FAKE, None)
+    assert call(P.scan_desc(2, 16, 64, 32)) == ESHAPE          # N > 16
+    assert call(P.scan_desc(2, 16, 64, 16, chunk=8)) == ESHAPE  # one pass only
+    assert call(P.scan_desc(2, 16, 64, 16, h0_batch_stride=64 * 16)) == ESTRIDE  # < 2 D N
+    assert call(P.scan_desc(2, 16, 64, 16), Aim=None) == ENULL
+    assert call(P.scan_desc(2, 16, 64, 16), x=None) == ENULL
+    assert call(P.scan_desc(2, 16, 60, 16)) == EALIGN
+    assert call(P.scan_desc(2, 16, 64, 16), h0=FAKE + 4) == EALIGN
+    assert call(P.scan_desc(0, 16, 64, 16)) == OK
+
+
 def test_topk_validation_errors():
     L = P.lib()
     ws = P.retrieve_workspace_bytes(4, 10, 16)

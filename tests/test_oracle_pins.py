@@ -426,3 +426,57 @@ def test_smc_planted_routes():
     emb, dom, sub, pm, pj = synth.smc_inputs_host(64, 384, 5, 4, seed=7)
     m, j = oracle.route2(emb, dom, sub)
     assert np.array_equal(m, pm.numpy()) and np.array_equal(j, pj.numpy())
+
+
+# --------------------------------------------------------------------------
+# Complex diagonal A (Sec. 3: A_k has an imaginary part pi k)
+# --------------------------------------------------------------------------
+def test_complex_scan_with_zero_frequency_is_the_real_scan():
+    inp = _rand(2, 40, 5, 4, seed=27, h0_std=0.7)
+    h0c = np.stack([np.asarray(inp["h0"]), np.zeros_like(np.asarray(inp["h0"]))], axis=-1)
+    y_c, h_c = oracle.scan_complex(inp["x"], inp["dt"], inp["A"], np.zeros_like(inp["A"]),
+                                   inp["B"], inp["C"], inp["z"], inp["Dskip"], h0c)
+    y_r, h_r = oracle.scan(inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                           inp["Dskip"], inp["h0"])
+    assert np.array_equal(y_c, y_r)
+    assert np.array_equal(h_c[..., 0], h_r) and not np.any(h_c[..., 1])
+
+
+def test_complex_scan_geometric_closed_form():
+    """Constant dt, B, x: h_L = alpha^L h0 + beta (1 - alpha^L) / (1 - alpha)
+    with the complex alpha = exp(-dt (a + i w)), beta = dt B x; the readout
+    takes the real part.  D != N so a transposed A or w fails."""
+    L, D, N = 300, 3, 5
+    g = np.random.default_rng(28)
+    dt, xv = 0.07, 0.9
+    a = g.uniform(1, 16, (D, N))
+    w = np.pi * np.arange(N)[None, :] * np.ones((D, 1)) + g.uniform(-1, 1, (D, N))
+    Bv = g.normal(0, 0.5, N)
+    Cv = g.normal(0, 0.5, N)
+    h0 = g.normal(size=(1, D, N)) + 1j * g.normal(size=(1, D, N))
+    x = np.full((1, L, D), xv)
+    dts = np.full((1, L, D), dt)
+    Bm = np.tile(Bv, (1, L, 1))
+    Cm = np.tile(Cv, (1, L, 1))
+    y, hT = oracle.scan_complex(x, dts, a, w, Bm, Cm, None, None,
+                                np.stack([h0.real, h0.imag], axis=-1))
+    alpha = np.exp(-dt * (a + 1j * w))
+    beta = dt * Bv[None, :] * xv
+    ref = alpha ** L * h0[0] + beta * (1 - alpha ** L) / (1 - alpha)
+    assert np.allclose(hT[0, ..., 0], ref.real, rtol=0, atol=1e-12)
+    assert np.allclose(hT[0, ..., 1], ref.imag, rtol=0, atol=1e-12)
+    assert np.allclose(y[0, -1], (ref.real * Cv[None, :]).sum(axis=1), rtol=0, atol=1e-12)
+
+
+def test_complex_scan_pure_rotation():
+    """No decay and no input: each state turns by -w * sum(dt), |h| is kept."""
+    L, D, N = 50, 2, 3
+    g = np.random.default_rng(29)
+    dts = g.uniform(0.01, 0.3, (1, L, D))
+    w = g.uniform(-5, 5, (D, N))
+    h0 = g.normal(size=(1, D, N)) + 1j * g.normal(size=(1, D, N))
+    _, hT = oracle.scan_complex(np.zeros((1, L, D)), dts, np.zeros((D, N)), w,
+                                np.zeros((1, L, N)), None, None, None,
+                                np.stack([h0.real, h0.imag], axis=-1), want_y=False)
+    ref = h0[0] * np.exp(-1j * w * dts[0].sum(axis=0)[:, None])
+    assert np.allclose(hT[0, ..., 0] + 1j * hT[0, ..., 1], ref, rtol=0, atol=1e-12)
