@@ -53,6 +53,14 @@ constexpr int kPF = PRECOG_SCAN_PF;  // time steps of inputs per pipeline tile
 
 enum Kind { kReadout = 0, kStateOnly = 1, kSummary = 2 };
 
+// B_t and C_t reach the lanes through LDS (1) or DPP row broadcasts (0); see
+// the kernel.
+#ifndef PRECOG_SCAN_LDS_BCAST
+#define PRECOG_SCAN_LDS_BCAST 1
+#endif
+constexpr bool kLdsBcast = PRECOG_SCAN_LDS_BCAST != 0;
+
+
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16_t v) {
   return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
@@ -217,6 +225,16 @@ __device__ __forceinline__ void token_group(float (&h)[N], const float (&a2)[N],
   if constexpr (READOUT) readout_group<N, g>(acc, cv, h);
 }
 
+// One token for 16 states with B_t / C_t already in VGPRs (the same value in
+// every lane): the same arithmetic, in the same order, as token_group.
+template <int N, bool READOUT, int... m>
+__device__ __forceinline__ void token_vgpr(float (&h)[N], const float (&a2)[N], float dtv, float u,
+                                           const float (&bl)[16], const float (&cl)[16], float& acc,
+                                           std::integer_sequence<int, m...>) {
+  ((h[m] = fmaf(__builtin_amdgcn_exp2f(dtv * a2[m]), h[m], u * bl[m])), ...);
+  if constexpr (READOUT) ((acc = fmaf(cl[m], h[m], acc)), ...);
+}
+
 template <int N, bool READOUT, int... g>
 __device__ __forceinline__ void token(float (&h)[N], const float (&a2)[N], float dtv, float u,
                                       const float (&bv)[(N + 15) / 16], const float (&cv)[(N + 15) / 16],
@@ -348,6 +366,34 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     typename SI::raw x[kPF], dt[kPF], z[kPF], b[kPF][G], c[kPF][G];
   };
   Tile t0b, t1b;
+
+  // With 16 states per lane, B_t / C_t of a tile are written (as fp32) to a
+  // wave-private LDS slice when the tile is consumed, by the lanes that
+  // loaded them, and each token reads its 16 (+16) coefficients back with
+  // same-address (broadcast) 16-byte reads into VGPRs, so the state update
+  // and the readout use plain VALU operands instead of DPP broadcasts.  The
+  // slice is private to the wave: no barrier.
+  // Used where it was measured to pay: with a readout (32 broadcasts per
+  // token replaced), or when a channel spans several lanes (N > 16); a
+  // readout-free N = 16 scan saves only the 16 B broadcasts, less than the
+  // staging costs.
+  constexpr bool kLds = kLdsBcast && NL == 16 && (kRead || P > 1);
+  __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
+  auto stage = [&](const Tile& tb) {
+    if constexpr (kLds) {
+      if ((lane >> 4) < P) {
+#pragma unroll
+        for (int k = 0; k < kPF; ++k) {
+          bc_lds[wave][k][0][16 * grp + lane16] = SI::f32(tb.b[k][0]);
+          if constexpr (kRead) bc_lds[wave][k][1][16 * grp + lane16] = SI::f32(tb.c[k][0]);
+        }
+      }
+      // Wait until the writes have completed (lgkmcnt(0); vmcnt and expcnt
+      // untouched) before any lane reads the tile: without this explicit
+      // wait, tail tiles were computed with stale coefficients.
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+    }
+  };
   const int last = nsteps > 0 ? nsteps - 1 : 0;
   auto fetch = [&](Tile& tb, int tile) {
 #pragma unroll
@@ -367,19 +413,44 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     }
   };
 
+  // coefficients of the current token, read from the staged tile
+  struct Coef {
+    float b[16], c[16];
+  };
+  // Read as float, the type the values were stored with, so the compiler
+  // sees the reads and the staging writes as possibly aliasing and keeps
+  // their order (a vector-typed read could be reordered across the writes
+  // of the next tile); consecutive aligned reads still merge into
+  // ds_read_b128.
+  auto read_coef = [&](Coef& cd, int k) {
+    if constexpr (kLds) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        cd.b[j] = bc_lds[wave][k][0][16 * grp + j];
+        cd.c[j] = kRead ? bc_lds[wave][k][1][16 * grp + j] : 0.f;
+      }
+    }
+  };
+
   float dtacc = 0.f;
   auto step = [&](const Tile& tb, int k, int st) {
     const float xv = SI::f32(tb.x[k]);
     const float dtv = SI::f32(tb.dt[k]);
-    float cv[G];
-#pragma unroll
-    for (int j = 0; j < G; ++j) cv[j] = kRead ? SI::f32(tb.c[k][j]) : 0.f;
     const float u = dtv * xv;
     float acc = 0.f;
-    float bv[G];
+    if constexpr (kLds) {
+      Coef cf;
+      read_coef(cf, k);
+      token_vgpr<NL, kRead>(h, a2, dtv, u, cf.b, cf.c, acc, std::make_integer_sequence<int, 16>{});
+    } else {
+      float cv[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) bv[j] = SI::f32(tb.b[k][j]);
-    token<NL, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
+      for (int j = 0; j < G; ++j) cv[j] = kRead ? SI::f32(tb.c[k][j]) : 0.f;
+      float bv[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) bv[j] = SI::f32(tb.b[k][j]);
+      token<NL, kRead>(h, a2, dtv, u, bv, cv, acc, std::make_integer_sequence<int, G>{});
+    }
     if constexpr (kRead) {
       // sum the P groups' partial readouts (lanes 16 and 32 apart)
       if constexpr (P >= 2) acc += lane_xor(acc, 16);
@@ -407,10 +478,12 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     }
   };
   auto run_tile = [&](const Tile& tb, int tile) {
+    stage(tb);
 #pragma unroll
     for (int k = 0; k < kPF; ++k) step(tb, k, tile * kPF + k);
   };
   auto run_tile_guarded = [&](const Tile& tb, int tile) {
+    stage(tb);
 #pragma unroll
     for (int k = 0; k < kPF; ++k)
       if (tile * kPF + k < nsteps) step(tb, k, tile * kPF + k);
