@@ -253,49 +253,6 @@ __device__ __forceinline__ bool better(double s, int64_t i, double bs, int64_t b
 
 constexpr int kMaxE = 4096;
 
-// fp64 score of key row ii against the query in qs: the wave stages the row
-// in rs, lane 0 sums the exact products in feature order (fma equals
-// multiply-then-add here: the product of two fp32 values is exact in fp64),
-// reading eight float4 pairs per LDS round trip, and every lane gets the sum.
-__device__ __forceinline__ double exact_score(const RetrieveParams& p, const float4* qs, float4* rs,
-                                             int64_t ii, int lane, int E) {
-  const float4* kr = reinterpret_cast<const float4*>(p.K + ii * p.E);
-  __syncthreads();  // previous row consumed (and qs complete)
-#pragma unroll 4
-  for (int e4 = lane; e4 < E / 4; e4 += 64) rs[e4] = kr[e4];
-  __syncthreads();
-  double s = 0.0;
-  if (lane == 0) {
-    int e4 = 0;
-    for (; e4 + 8 <= E / 4; e4 += 8) {
-      float4 a[8], b[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        a[j] = qs[e4 + j];
-        b[j] = rs[e4 + j];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        s = fma(static_cast<double>(a[j].x), static_cast<double>(b[j].x), s);
-        s = fma(static_cast<double>(a[j].y), static_cast<double>(b[j].y), s);
-        s = fma(static_cast<double>(a[j].z), static_cast<double>(b[j].z), s);
-        s = fma(static_cast<double>(a[j].w), static_cast<double>(b[j].w), s);
-      }
-    }
-    for (; e4 < E / 4; ++e4) {
-      const float4 a = qs[e4];
-      const float4 b = rs[e4];
-      s = fma(static_cast<double>(a.x), static_cast<double>(b.x), s);
-      s = fma(static_cast<double>(a.y), static_cast<double>(b.y), s);
-      s = fma(static_cast<double>(a.z), static_cast<double>(b.z), s);
-      s = fma(static_cast<double>(a.w), static_cast<double>(b.w), s);
-    }
-  }
-  const int lo = __builtin_amdgcn_readfirstlane(static_cast<int>(__double2loint(s)));
-  const int hi = __builtin_amdgcn_readfirstlane(static_cast<int>(__double2hiint(s)));
-  return __hiloint2double(hi, lo);
-}
-
 __device__ __forceinline__ double shfl_d(double v, int src_lane) {
   const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2loint(v)));
   const int hi = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2hiint(v)));
@@ -312,22 +269,31 @@ __device__ __forceinline__ bool before(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
+constexpr int kCand = 64;             // candidate list capacity (indices)
+constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
+
 // decide: one 64-lane workgroup per query (see the file comment).  For the
 // k best keys the bound uses t_k, the k-th largest block maximum: k distinct
 // blocks hold a key with screen score >= t_k, so k keys have exact scores
 // >= t_k - e_max and every key of the exact top k has S~_i + e(i) >= that.
 // (k = 1: t_1 = m.)  Blocks are discarded with their maxima and norm bounds,
-// then keys one by one; candidates are scored exactly and kept in a list
+// then keys one by one; surviving keys are collected in an LDS list and
+// scored exactly in batches: the wave stages a batch of rows in LDS (row
+// pitch E + 1 words, so lanes reading different rows hit different banks)
+// and lane j sums row j in fp64 in feature order (fma equals
+// multiply-then-add here: the product of two fp32 values is exact in fp64),
+// so the chains of a batch run side by side.  Scores enter a rank list
 // spread over the lanes (lane j holds rank j), ordered by score, then by
-// lower index.
+// lower index; the order of insertion does not change the list.
 __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const int64_t q = blockIdx.x;
   const int lane = threadIdx.x;
   const int E = static_cast<int>(p.E);
   const int nkb = p.nkb;
   const int k = p.k;
-  __shared__ float4 qs[kMaxE / 4];
-  __shared__ float4 rs[kMaxE / 4];
+  __shared__ float qs[kMaxE];
+  __shared__ float rs[kRowWords];
+  __shared__ int cand[kCand];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
   const float* bm = p.blockmax + q * nkb;
   const float* sc = p.scores + q * p.ld_scores;
@@ -336,28 +302,18 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
 #pragma unroll 4
   for (int e4 = lane; e4 < E / 4; e4 += 64) {
     const float4 v = qg4[e4];
-    qs[e4] = v;
+    qs[4 * e4] = v.x;
+    qs[4 * e4 + 1] = v.y;
+    qs[4 * e4 + 2] = v.z;
+    qs[4 * e4 + 3] = v.w;
     nq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, nq))));
   }
-  // largest block norm, 256 blocks per round trip
-  float nmax = 0.f;
-  for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
-    float n[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int kb = kb0 + 64 * j + lane;
-      n[j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) nmax = fmaxf(nmax, n[j]);
-  }
   const float qnorm = sqrtf(wave_sum(nq));
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) nmax = fmaxf(nmax, xor_shfl(nmax, s));
 
   // t_k: k rounds, each taking the first (value, index) pair after the
-  // previous one; fewer than k ranked blocks leave t_k = -inf (every key is
-  // then a candidate)
+  // previous one (the first round also takes the largest block norm); fewer
+  // than k ranked blocks leave t_k = -inf (every key is then a candidate)
+  float nmax = 0.f;
   float tv = INFINITY;
   int ti = -1;
   bool found = true;
@@ -366,15 +322,17 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     int bi = 0x7fffffff;
     bool any = false;
     for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
-      float b[4];
+      float b[4], n[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kb = kb0 + 64 * j + lane;
         b[j] = kb < nkb ? bm[kb] : __builtin_nanf("");
+        n[j] = (r == 0 && kb < nkb) ? p.blocknorm2[kb] : 0.f;
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kb = kb0 + 64 * j + lane;
+        nmax = fmaxf(nmax, n[j]);
         if (before(tv, ti, b[j], kb) && (!any || before(b[j], kb, bv, bi))) {
           bv = b[j];
           bi = kb;
@@ -399,6 +357,8 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
       ti = bi;
     }
   }
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) nmax = fmaxf(nmax, xor_shfl(nmax, s));
   const float tk = found ? tv : -INFINITY;
 
   // Screen-score error bound per unit of |q| |k_i|: dropped split terms
@@ -418,6 +378,61 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   // rank list: lane j < k holds the j-th best (score, index) so far
   double ls = -INFINITY;
   int64_t li = -1;
+  auto insert = [&](double s, int64_t ii) {
+    const bool ahead = lane < k && li >= 0 && better(ls, li, s, ii);
+    const int pos = __builtin_popcountll(__ballot(ahead));
+    if (pos < k) {
+      const double ps = shfl_d(ls, lane > 0 ? lane - 1 : 0);
+      const int pil = shfl_i(static_cast<int>(li), lane > 0 ? lane - 1 : 0);
+      if (lane > pos) {
+        ls = ps;
+        li = pil;
+      } else if (lane == pos) {
+        ls = s;
+        li = ii;
+      }
+    }
+  };
+
+  // exact scores of the listed candidates, a batch of rows at a time
+  const int pitch = E + 1;
+  const int batch_max = kRowWords / pitch < 64 ? kRowWords / pitch : 64;
+  int ncand = 0;
+  auto flush = [&]() {
+    for (int c0 = 0; c0 < ncand; c0 += batch_max) {
+      const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
+      __syncthreads();  // previous batch consumed, list and qs complete
+      // one flat (row, float4) space, so the loads of several rows are in
+      // flight together
+      const int e4n = E / 4;
+#pragma unroll 8
+      for (int f = lane; f < nb * e4n; f += 64) {
+        const int r = f / e4n;
+        const int e4 = f - r * e4n;
+        const float4 v =
+            reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4];
+        float* dst = rs + r * pitch + 4 * e4;
+        dst[0] = v.x;
+        dst[1] = v.y;
+        dst[2] = v.z;
+        dst[3] = v.w;
+      }
+      __syncthreads();
+      double s = 0.0;
+      if (lane < nb) {
+        const float* row = rs + lane * pitch;
+        for (int e = 0; e < E; ++e)
+          s = fma(static_cast<double>(qs[e]), static_cast<double>(row[e]), s);
+      }
+      for (int r = 0; r < nb; ++r) {
+        const int lo = __builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(__double2loint(s)));
+        const int hi = __builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(__double2hiint(s)));
+        insert(__hiloint2double(hi, lo), cand[c0 + r]);
+      }
+    }
+    ncand = 0;
+  };
+
   for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
     uint64_t bmask[4];
 #pragma unroll
@@ -437,32 +452,18 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
         const int blk = kb0 + 64 * j + __builtin_ctzll(bmask[j]);
         bmask[j] &= bmask[j] - 1;
         const int64_t i = static_cast<int64_t>(blk) * kKB + (lane & (kKB - 1));
-        bool cand = false;
+        bool cand_ok = false;
         if (lane < kKB && i < p.M)
-          cand = static_cast<double>(sc[i]) + gq * sqrt(static_cast<double>(p.rownorm2[i])) + tiny >= thresh;
-        uint64_t cmask = __ballot(cand);
-        while (cmask) {
-          const int64_t ii = static_cast<int64_t>(blk) * kKB + __builtin_ctzll(cmask);
-          cmask &= cmask - 1;
-          const double s = exact_score(p, qs, rs, ii, lane, E);
-          // insert at the number of held entries that rank before it
-          const bool ahead = lane < k && li >= 0 && better(ls, li, s, ii);
-          const int pos = __builtin_popcountll(__ballot(ahead));
-          if (pos < k) {
-            const double ps = shfl_d(ls, lane > 0 ? lane - 1 : 0);
-            const int pil = shfl_i(static_cast<int>(li), lane > 0 ? lane - 1 : 0);
-            if (lane > pos) {
-              ls = ps;
-              li = pil;
-            } else if (lane == pos) {
-              ls = s;
-              li = ii;
-            }
-          }
-        }
+          cand_ok = static_cast<double>(sc[i]) + gq * sqrt(static_cast<double>(p.rownorm2[i])) + tiny >= thresh;
+        const uint64_t cmask = __ballot(cand_ok);
+        if (!cmask) continue;
+        if (ncand + kKB > kCand) flush();
+        if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(i);
+        ncand += __builtin_popcountll(cmask);
       }
     }
   }
+  flush();
   if (lane < k) {
     p.idx[q * k + lane] = static_cast<int32_t>(li);
     if (p.score) p.score[q * k + lane] = ls;
