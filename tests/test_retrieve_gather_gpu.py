@@ -121,3 +121,22 @@ def test_query_time_path_end_to_end():
                                inp["Dskip"], h0_ref, nthreads=8)
     assert err_rms(y.double().cpu().numpy(), y_ref) <= TOL_BF16
     assert err_rms(hT.double().cpu().numpy(), h_ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("Q,M,E", [(40, 300, 4096), (7, 5, 64), (8, 100000, 384)])
+def test_retrieval_extreme_shapes(Q, M, E):
+    """The largest feature count (4096: one candidate row per rescoring
+    batch), a single partial key block, and a 100,000-key index."""
+    q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 3), seed=Q + M + E)
+    ref, _ = oracle.top1(q, K, nthreads=8)
+    assert np.array_equal(_gpu_top1(q, K), ref)
+
+
+def test_gather_more_queries_than_one_grid_dimension():
+    """Q = 70,000 > 65,535: the launches walk the queries in slices."""
+    store = synth.state_store(10, 16, seed=12).to(DEV)
+    idx = torch.from_numpy(np.random.default_rng(2).integers(0, 10, 70000).astype(np.int32)).to(DEV)
+    h0 = P.gather(store, idx, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.gather(store.cpu(), idx.cpu().numpy())
+    assert np.array_equal(h0.double().cpu().numpy(), ref)

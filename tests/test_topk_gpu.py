@@ -163,3 +163,24 @@ def test_topk_query_path_end_to_end():
                                inp["Dskip"], h0_ref, nthreads=8)
     assert err_rms(y.double().cpu().numpy(), y_ref) <= TOL_BF16
     assert err_rms(hT.double().cpu().numpy(), h_ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("Q,M,E,k", [(20, 300, 4096, 5), (9, 7, 16, 7)])
+def test_topk_extreme_shapes(Q, M, E, k):
+    """E = 4096 (one candidate row per rescoring batch) and k = M (every key
+    ranked) on a single partial key block."""
+    q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 3), seed=Q * 3 + M + E)
+    _check_topk(q, K, k)
+
+
+def test_compose_more_queries_than_one_grid_dimension():
+    store = synth.state_store(12, 16, seed=13).to(DEV)
+    g = np.random.default_rng(3)
+    idx = torch.from_numpy(g.integers(0, 12, (70000, 2)).astype(np.int32)).to(DEV)
+    sc = torch.from_numpy(g.normal(size=(70000, 2))).to(DEV)
+    h0 = P.compose(store, idx, sc, tau=0.5, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    idx_n, sc_n = idx.cpu().numpy(), sc.cpu().numpy()
+    ref = oracle.topk_compose(store.cpu(), idx_n[-500:], sc_n[-500:], 0.5)
+    bound = _compose_bound(store.double().cpu().numpy(), idx_n[-500:], sc_n[-500:], 0.5)
+    assert np.all(np.abs(h0[-500:].double().cpu().numpy() - ref) <= bound)
