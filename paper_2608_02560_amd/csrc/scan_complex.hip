@@ -111,14 +111,14 @@ __global__ __launch_bounds__(kBlock) void scan_complex_kernel(
   const uint32_t el = static_cast<uint32_t>(lane16 < N ? lane16 : N - 1) * sizeof(TIn);
 
   struct Tile {
-    typename SI::raw x[kPF], dt[kPF], z[kPF], b[kPF], c[kPF];
+    typename SI::raw x[kPFWide], dt[kPFWide], z[kPFWide], b[kPFWide], c[kPFWide];
   };
   Tile t0b, t1b;
   const int last = nsteps > 0 ? nsteps - 1 : 0;
   auto fetch = [&](Tile& tb, int tile) {
 #pragma unroll
-    for (int k = 0; k < kPF; ++k) {
-      int st = tile * kPF + k;
+    for (int k = 0; k < kPFWide; ++k) {
+      int st = tile * kPFWide + k;
       st = st < last ? st : last;
       const uint32_t so = static_cast<uint32_t>(st) * in_row;
       tb.x[k] = SI::load(rx, dl, so);
@@ -148,18 +148,18 @@ __global__ __launch_bounds__(kBlock) void scan_complex_kernel(
   };
   auto run_tile = [&](const Tile& tb, int tile) {
 #pragma unroll
-    for (int k = 0; k < kPF; ++k) step(tb, k, tile * kPF + k);
+    for (int k = 0; k < kPFWide; ++k) step(tb, k, tile * kPFWide + k);
   };
   auto run_tile_guarded = [&](const Tile& tb, int tile) {
 #pragma unroll
-    for (int k = 0; k < kPF; ++k)
-      if (tile * kPF + k < nsteps) step(tb, k, tile * kPF + k);
+    for (int k = 0; k < kPFWide; ++k)
+      if (tile * kPFWide + k < nsteps) step(tb, k, tile * kPFWide + k);
   };
 
   if (nsteps > 0) {
     fetch(t0b, 0);
     int tile = 0;
-    for (; (tile + 2) * kPF <= nsteps; tile += 2) {
+    for (; (tile + 2) * kPFWide <= nsteps; tile += 2) {
       fetch(t1b, tile + 1);
       run_tile(t0b, tile);
       fetch(t0b, tile + 2);

@@ -46,10 +46,18 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBlock = 256;  // 4 waves: 256 adjacent channels of one row
+// Time steps of inputs per pipeline tile.  The plain scan kinds use 4: it
+// keeps the readout kernel at 121 VGPRs (4 waves per SIMD), which lets short
+// launches such as a 32-token query prefill over 4096 waves run in one round
+// and helps the chunked passes, at no cost to the corpus encode (2 waves per
+// SIMD either way).  Trajectory capture keeps 8: its state stores share the
+// vector-memory counter with the tile loads, and longer tiles wait on them
+// less often.
 #ifndef PRECOG_SCAN_PF
-#define PRECOG_SCAN_PF 8
+#define PRECOG_SCAN_PF 4
 #endif
-constexpr int kPF = PRECOG_SCAN_PF;  // time steps of inputs per pipeline tile
+constexpr int kPFPlain = PRECOG_SCAN_PF;
+constexpr int kPFWide = 8;  // trajectory capture, complex-A kernel
 
 enum Kind { kReadout = 0, kStateOnly = 1, kSummary = 2 };
 
@@ -280,6 +288,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   constexpr int NL = N / P;                // states held by one lane
   constexpr int G = (NL + 15) / 16;        // registers per token for B_t (and C_t)
   constexpr int kChan = kBlock / P;        // channels per workgroup
+  constexpr int kPF = TRAJ ? kPFWide : kPFPlain;
   constexpr bool kRead = KIND == kReadout;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int dblk = lb % p.dblocks;
