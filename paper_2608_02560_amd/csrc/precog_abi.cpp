@@ -17,8 +17,12 @@ namespace {
 constexpr int kMaxDevices = 64;
 // 0 = unknown, 1 = gfx950, 2 = other architecture
 std::atomic<int> g_arch_ok[kMaxDevices];
+// compute units of each device (0 = not yet queried)
+std::atomic<int> g_cus[kMaxDevices];
 
-precog_status check_device() {
+// Checks that the current device is a gfx950; `cus`, if given, receives its
+// compute-unit count.  Both are queried once per device and cached.
+precog_status check_device(int* cus = nullptr) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return PRECOG_ERR_HIP;
   if (dev < 0 || dev >= kMaxDevices) return PRECOG_ERR_ARCH;
@@ -27,8 +31,11 @@ precog_status check_device() {
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return PRECOG_ERR_HIP;
     st = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_cus[dev].store(prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1,
+                     std::memory_order_relaxed);
     g_arch_ok[dev].store(st, std::memory_order_relaxed);
   }
+  if (cus) *cus = g_cus[dev].load(std::memory_order_relaxed);
   return st == 1 ? PRECOG_OK : PRECOG_ERR_ARCH;
 }
 
@@ -38,7 +45,8 @@ bool valid_n(int64_t n) {
   return n == 1 || n == 2 || n == 4 || n == 8 || n == 16 || n == 32 || n == 64;
 }
 
-constexpr int64_t kBlock = 256;           // channels per scan workgroup
+constexpr int64_t kBlock = precog::kScanThreads;  // lanes per real-A scan workgroup
+constexpr int64_t kComplexBlock = 256;             // lanes per complex-A scan workgroup
 constexpr int64_t kTargetWaves = 2048;    // 2 waves per SIMD on 256 CUs
 constexpr int64_t kMinAutoChunk = 64;
 
@@ -172,7 +180,8 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   if (dblocks * Bt * nchunks > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   if (Bt * D * N / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
 
-  st = check_device();
+  int cus = 1;
+  st = check_device(&cus);
   if (st != PRECOG_OK) return st;
 
   precog::ScanParams p{};
@@ -199,6 +208,11 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   p.dblocks = static_cast<int>(dblocks);
   p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
             (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
+  // Progress balancing between the two waves of a SIMD pays when every wave
+  // of the launch is resident from the start (at most 4 per SIMD); in launches
+  // of many rounds it was measured to cost time, so it is left off there.
+  const int64_t final_waves = dblocks * Bt * nchunks * (kBlock / 64);
+  if (final_waves <= 4LL * 4 * cus) p.flags |= precog::kBalance;
   p.traj = traj;
   p.traj_every = traj ? every : 1;
   p.traj_count = traj_count;
@@ -492,7 +506,7 @@ precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, c
   const void* ptrs[] = {x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
-  const int64_t dblocks = ceil_div(D, kBlock);
+  const int64_t dblocks = ceil_div(D, kComplexBlock);
   if (dblocks * Bt > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   st = check_device();
   if (st != PRECOG_OK) return st;

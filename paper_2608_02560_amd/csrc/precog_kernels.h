@@ -16,6 +16,7 @@ enum ScanFlags : int {
   kHasD = 2,   // Dskip present
   kHasH0 = 4,  // initial state present
   kHasHT = 8,  // final state requested
+  kBalance = 16,  // balance the progress of waves sharing a SIMD (scan_kernel)
 };
 
 // Everything one scan launch needs.  Passed by value as the kernel argument.
@@ -42,6 +43,14 @@ struct ScanParams {
   int dblocks;    // ceil(D / 256)
   int flags;
 };
+
+// Threads per workgroup of the real-A scan kernels: 8 waves, so that the two
+// waves sharing a SIMD at two waves per SIMD belong to one workgroup and can
+// see each other's progress in LDS (see scan_kernels.h).
+#ifndef PRECOG_SCAN_WG
+#define PRECOG_SCAN_WG 512
+#endif
+constexpr int kScanThreads = PRECOG_SCAN_WG;
 
 // Launchers (return the HIP launch status).  in/out/state dtypes are the
 // precog_dtype codes of the public header.

@@ -45,7 +45,14 @@ namespace precog {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBlock = 256;  // 4 waves: 256 adjacent channels of one row
+constexpr int kBlock = 256;              // complex-A kernel: 4 waves, 256 channels of one row
+constexpr int kSBlock = kScanThreads;    // real-A scan kernels: 8 waves
+
+// Progress balancing between the waves of a workgroup that share a SIMD
+// (see scan_kernel).
+#ifndef PRECOG_SCAN_FAIR
+#define PRECOG_SCAN_FAIR 1
+#endif
 // Time steps of inputs per pipeline tile.  The plain scan kinds use 4: it
 // keeps the readout kernel at 121 VGPRs (4 waves per SIMD), which lets short
 // launches such as a 32-token query prefill over 4096 waves run in one round
@@ -277,7 +284,7 @@ __device__ __forceinline__ float lane_xor(float v, int m) {
 // read other lanes); lanes past D compute on clamped channels and store
 // nothing.
 template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, bool TRAJ>
-__global__ __launch_bounds__(kBlock) void scan_kernel(
+__global__ __launch_bounds__(kSBlock) void scan_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
     const ScanParams p) {
@@ -287,7 +294,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   constexpr int P = kLanesPerChannel<N>;
   constexpr int NL = N / P;                // states held by one lane
   constexpr int G = (NL + 15) / 16;        // registers per token for B_t (and C_t)
-  constexpr int kChan = kBlock / P;        // channels per workgroup
+  constexpr int kChan = kSBlock / P;       // channels per workgroup
   constexpr int kPF = TRAJ ? kPFWide : kPFPlain;
   constexpr bool kRead = KIND == kReadout;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
@@ -301,6 +308,24 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const int grp = (lane >> 4) % P;  // this lane's state group
   // channel of this lane: 16 per row, rows of one channel set are P apart
   const int64_t wave_d0 = static_cast<int64_t>(dblk) * kChan + wave * (64 / P);
+
+  // Progress balancing (launches whose waves are all resident at once; the
+  // host sets kBalance).  Waves are placed on the four SIMDs of a CU in
+  // order, so waves w and w + 4 of a workgroup share one.  Issue arbitration
+  // between waves of equal priority favours the older one, so with equal
+  // work one of the two would run well ahead and the other would finish its
+  // sequence alone on the SIMD, where a single wave issues at about half the
+  // rate of two.  Instead each wave publishes its tile count in LDS and, at
+  // every tile, takes priority 0 while ahead of its partner and 1 otherwise,
+  // so the two advance together.  (Dead waves stay at 0; their live partners
+  // then run at priority 0, which changes nothing.)
+  constexpr int kWaves = kSBlock / 64;
+  const bool fair = PRECOG_SCAN_FAIR != 0 && kWaves == 8 && (p.flags & kBalance) != 0;
+  __shared__ int progress[kWaves];
+  if (fair) {  // uniform over the workgroup
+    __atomic_store_n(&progress[wave], 0, __ATOMIC_RELAXED);
+    __syncthreads();  // before any wave can leave
+  }
   if (wave_d0 >= D) return;  // whole wave past the last channel
   const int64_t dtrue = wave_d0 + (lane & 15) + 16 * (lane / (16 * P));
   const bool live = dtrue < D;
@@ -387,7 +412,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   // readout-free N = 16 scan saves only the 16 B broadcasts, less than the
   // staging costs.
   constexpr bool kLds = kLdsBcast && NL == 16 && (kRead || P > 1);
-  __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
+  __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kSBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
   auto stage = [&](const Tile& tb) {
     if constexpr (kLds) {
       if ((lane >> 4) < P) {
@@ -486,6 +511,18 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
       }
     }
   };
+  // The balance check runs at the head of each iteration of the time loop
+  // (every 2 tiles), which is a block boundary anyway, so the unrolled body
+  // stays one straight-line block whether or not the launch balances.
+  auto balance = [&](int tile) {
+    __atomic_store_n(&progress[wave], tile, __ATOMIC_RELAXED);
+    const int other = __builtin_amdgcn_readfirstlane(
+        __atomic_load_n(&progress[wave ^ (kWaves / 2)], __ATOMIC_RELAXED));
+    if (tile > other)
+      __builtin_amdgcn_s_setprio(0);
+    else
+      __builtin_amdgcn_s_setprio(1);
+  };
   auto run_tile = [&](const Tile& tb, int tile) {
     stage(tb);
 #pragma unroll
@@ -503,6 +540,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     int tile = 0;
     // Pairs of whole tiles: straight-line code, no per-token guards.
     for (; (tile + 2) * kPF <= nsteps; tile += 2) {
+      if (fair) balance(tile);
       fetch(t1b, tile + 1);
       run_tile(t0b, tile);
       fetch(t0b, tile + 2);
@@ -571,7 +609,7 @@ hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
   if (p.nchunks > 1) {
     const int64_t g1 = rows_blocks * (p.nchunks - 1);
     hipLaunchKernelGGL((scan_kernel<N, TIn, float, float, kSummary, false, false>), dim3(static_cast<unsigned>(g1)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
     const int64_t lanes = p.B * p.D * N;
     hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
                        0, s, p, N);
@@ -579,13 +617,13 @@ hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
   const int64_t g3 = rows_blocks * p.nchunks;
   if (p.y != nullptr && (p.flags & kHasZ))
     hipLaunchKernelGGL((scan_kernel<N, TIn, TOut, TSt, kReadout, true, TRAJ>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else if (p.y != nullptr)
     hipLaunchKernelGGL((scan_kernel<N, TIn, TOut, TSt, kReadout, false, TRAJ>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else
     hipLaunchKernelGGL((scan_kernel<N, TIn, float, TSt, kStateOnly, false, TRAJ>), dim3(static_cast<unsigned>(g3)),
-                       dim3(kBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
   return hipGetLastError();
 }
 
