@@ -279,7 +279,7 @@ constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
 // (k = 1: t_1 = m.)  Blocks are discarded with their maxima and norm bounds,
 // then keys one by one; surviving keys are collected in an LDS list and
 // scored exactly in batches: the wave stages a batch of rows in LDS (row
-// pitch E + 1 words, so lanes reading different rows hit different banks)
+// pitch E + 4 words, 16-byte aligned)
 // and lane j sums row j in fp64 in feature order (fma equals
 // multiply-then-add here: the product of two fp32 values is exact in fp64),
 // so the chains of a batch run side by side.  Scores enter a rank list
@@ -291,8 +291,8 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const int E = static_cast<int>(p.E);
   const int nkb = p.nkb;
   const int k = p.k;
-  __shared__ float qs[kMaxE];
-  __shared__ float rs[kRowWords];
+  __shared__ __attribute__((aligned(16))) float qs[kMaxE];
+  __shared__ __attribute__((aligned(16))) float rs[kRowWords];
   __shared__ int cand[kCand];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
   const float* bm = p.blockmax + q * nkb;
@@ -302,10 +302,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
 #pragma unroll 4
   for (int e4 = lane; e4 < E / 4; e4 += 64) {
     const float4 v = qg4[e4];
-    qs[4 * e4] = v.x;
-    qs[4 * e4 + 1] = v.y;
-    qs[4 * e4 + 2] = v.z;
-    qs[4 * e4 + 3] = v.w;
+    *reinterpret_cast<float4*>(qs + 4 * e4) = v;
     nq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, nq))));
   }
   const float qnorm = sqrtf(wave_sum(nq));
@@ -395,7 +392,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   };
 
   // exact scores of the listed candidates, a batch of rows at a time
-  const int pitch = E + 1;
+  const int pitch = E + 4;  // E is a multiple of 4: rows stay 16-byte aligned
   const int batch_max = kRowWords / pitch < 64 ? kRowWords / pitch : 64;
   int ncand = 0;
   auto flush = [&]() {
@@ -411,18 +408,24 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
         const int e4 = f - r * e4n;
         const float4 v =
             reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4];
-        float* dst = rs + r * pitch + 4 * e4;
-        dst[0] = v.x;
-        dst[1] = v.y;
-        dst[2] = v.z;
-        dst[3] = v.w;
+        *reinterpret_cast<float4*>(rs + r * pitch + 4 * e4) = v;
       }
       __syncthreads();
+      // the chain stays one fma per feature in feature order; reading four
+      // features per 16-byte LDS access (the query's a broadcast) and
+      // unrolling lets the reads run ahead of the dependent fp64 chain
       double s = 0.0;
       if (lane < nb) {
         const float* row = rs + lane * pitch;
-        for (int e = 0; e < E; ++e)
-          s = fma(static_cast<double>(qs[e]), static_cast<double>(row[e]), s);
+#pragma unroll 4
+        for (int e = 0; e < E; e += 4) {
+          const float4 qv = *reinterpret_cast<const float4*>(qs + e);
+          const float4 rv = *reinterpret_cast<const float4*>(row + e);
+          s = fma(static_cast<double>(qv.x), static_cast<double>(rv.x), s);
+          s = fma(static_cast<double>(qv.y), static_cast<double>(rv.y), s);
+          s = fma(static_cast<double>(qv.z), static_cast<double>(rv.z), s);
+          s = fma(static_cast<double>(qv.w), static_cast<double>(rv.w), s);
+        }
       }
       for (int r = 0; r < nb; ++r) {
         const int lo = __builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(__double2loint(s)));
