@@ -45,8 +45,7 @@ bool valid_n(int64_t n) {
   return n == 1 || n == 2 || n == 4 || n == 8 || n == 16 || n == 32 || n == 64;
 }
 
-constexpr int64_t kBlock = precog::kScanThreads;  // lanes per real-A scan workgroup
-constexpr int64_t kComplexBlock = 256;             // lanes per complex-A scan workgroup
+constexpr int64_t kBlock = precog::kScanThreads;  // lanes per scan workgroup (real and complex A)
 constexpr int64_t kTargetWaves = 2048;    // 2 waves per SIMD on 256 CUs
 constexpr int64_t kMinAutoChunk = 64;
 
@@ -506,9 +505,10 @@ precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, c
   const void* ptrs[] = {x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
-  const int64_t dblocks = ceil_div(D, kComplexBlock);
+  const int64_t dblocks = ceil_div(D, kBlock);
   if (dblocks * Bt > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
-  st = check_device();
+  int cus = 1;
+  st = check_device(&cus);
   if (st != PRECOG_OK) return st;
 
   precog::ScanParams p{};
@@ -533,6 +533,9 @@ precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, c
   p.dblocks = static_cast<int>(dblocks);
   p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
             (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
+  // progress balancing when every wave is resident from the start (as for
+  // the real-A scan)
+  if (dblocks * Bt * (kBlock / 64) <= 4LL * 4 * cus) p.flags |= precog::kBalance;
   (void)hipGetLastError();
   const hipError_t e = precog::launch_scan_complex(p, static_cast<int>(N), desc->in_dtype,
                                                    desc->out_dtype, desc->state_dtype,

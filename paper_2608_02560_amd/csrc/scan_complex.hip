@@ -57,7 +57,7 @@ __device__ __forceinline__ void store_cstate(TSt* dst, const float (&hr)[N], con
 // One lane = one (b, d) channel over the whole sequence.  READOUT: y is
 // written (else state only); HASZ: gate present.
 template <int N, typename TIn, typename TOut, typename TSt, bool READOUT, bool HASZ>
-__global__ __launch_bounds__(kBlock) void scan_complex_kernel(
+__global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
     const ScanParams p) {
@@ -68,7 +68,11 @@ __global__ __launch_bounds__(kBlock) void scan_complex_kernel(
   const int64_t D = p.D;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t wave_d0 = static_cast<int64_t>(dblk) * kBlock + wave * 64;
+  const int64_t wave_d0 = static_cast<int64_t>(dblk) * kSBlock + wave * 64;
+  // progress balancing between the two waves of a SIMD (scan_kernels.h)
+  const bool fair = balance_enabled(p);
+  __shared__ int progress[kSWaves];
+  if (fair) balance_init(progress, wave);  // uniform over the workgroup
   if (wave_d0 >= D) return;
   const int64_t dtrue = wave_d0 + lane;
   const bool live = dtrue < D;
@@ -160,6 +164,7 @@ __global__ __launch_bounds__(kBlock) void scan_complex_kernel(
     fetch(t0b, 0);
     int tile = 0;
     for (; (tile + 2) * kPFWide <= nsteps; tile += 2) {
+      if (fair) balance_step(progress, wave, tile);
       fetch(t1b, tile + 1);
       run_tile(t0b, tile);
       fetch(t0b, tile + 2);
@@ -183,13 +188,13 @@ hipError_t launch_c(const ScanParams& p, hipStream_t s) {
   const TIn* BB = static_cast<const TIn*>(p.Bm);
   const TIn* CC = static_cast<const TIn*>(p.Cm);
   if (p.y != nullptr && (p.flags & kHasZ))
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, true>), grid, dim3(kBlock), 0, s,
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, true>), grid, dim3(kSBlock), 0, s,
                        X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else if (p.y != nullptr)
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, false>), grid, dim3(kBlock), 0, s,
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, false>), grid, dim3(kSBlock), 0, s,
                        X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, float, TSt, false, false>), grid, dim3(kBlock), 0, s,
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, float, TSt, false, false>), grid, dim3(kSBlock), 0, s,
                        X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
   return hipGetLastError();
 }

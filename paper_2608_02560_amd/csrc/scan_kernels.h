@@ -45,14 +45,43 @@ namespace precog {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBlock = 256;              // complex-A kernel: 4 waves, 256 channels of one row
-constexpr int kSBlock = kScanThreads;    // real-A scan kernels: 8 waves
+constexpr int kSBlock = kScanThreads;    // scan workgroups (real and complex A): 8 waves
 
 // Progress balancing between the waves of a workgroup that share a SIMD
 // (see scan_kernel).
 #ifndef PRECOG_SCAN_FAIR
 #define PRECOG_SCAN_FAIR 1
 #endif
+constexpr int kSWaves = kSBlock / 64;
+
+// Progress balancing (launches whose waves are all resident at once; the
+// host sets kBalance).  Waves are placed on the four SIMDs of a CU in order,
+// so waves w and w + 4 of an 8-wave workgroup share one.  Issue arbitration
+// between waves of equal priority favours the older one, so with equal work
+// one of the two would run well ahead and the other would finish its
+// sequence alone on the SIMD, where a single wave issues at about half the
+// rate of two.  Instead each wave publishes its tile count in LDS and, at
+// the head of each iteration of its time loop, takes priority 0 while ahead
+// of its partner and 1 otherwise, so the two advance together.  (Dead waves
+// stay at 0; their live partners then run at priority 0, which changes
+// nothing.)
+__device__ __forceinline__ bool balance_enabled(const ScanParams& p) {
+  return PRECOG_SCAN_FAIR != 0 && kSWaves == 8 && (p.flags & kBalance) != 0;
+}
+// Before any wave of the workgroup can leave: every wave starts at 0.
+__device__ __forceinline__ void balance_init(int* progress, int wave) {
+  __atomic_store_n(&progress[wave], 0, __ATOMIC_RELAXED);
+  __syncthreads();
+}
+__device__ __forceinline__ void balance_step(int* progress, int wave, int tile) {
+  __atomic_store_n(&progress[wave], tile, __ATOMIC_RELAXED);
+  const int other = __builtin_amdgcn_readfirstlane(
+      __atomic_load_n(&progress[wave ^ (kSWaves / 2)], __ATOMIC_RELAXED));
+  if (tile > other)
+    __builtin_amdgcn_s_setprio(0);
+  else
+    __builtin_amdgcn_s_setprio(1);
+}
 // Time steps of inputs per pipeline tile.  The plain scan kinds use 4: it
 // keeps the readout kernel at 121 VGPRs (4 waves per SIMD), which lets short
 // launches such as a 32-token query prefill over 4096 waves run in one round
@@ -309,23 +338,10 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // channel of this lane: 16 per row, rows of one channel set are P apart
   const int64_t wave_d0 = static_cast<int64_t>(dblk) * kChan + wave * (64 / P);
 
-  // Progress balancing (launches whose waves are all resident at once; the
-  // host sets kBalance).  Waves are placed on the four SIMDs of a CU in
-  // order, so waves w and w + 4 of a workgroup share one.  Issue arbitration
-  // between waves of equal priority favours the older one, so with equal
-  // work one of the two would run well ahead and the other would finish its
-  // sequence alone on the SIMD, where a single wave issues at about half the
-  // rate of two.  Instead each wave publishes its tile count in LDS and, at
-  // every tile, takes priority 0 while ahead of its partner and 1 otherwise,
-  // so the two advance together.  (Dead waves stay at 0; their live partners
-  // then run at priority 0, which changes nothing.)
-  constexpr int kWaves = kSBlock / 64;
-  const bool fair = PRECOG_SCAN_FAIR != 0 && kWaves == 8 && (p.flags & kBalance) != 0;
-  __shared__ int progress[kWaves];
-  if (fair) {  // uniform over the workgroup
-    __atomic_store_n(&progress[wave], 0, __ATOMIC_RELAXED);
-    __syncthreads();  // before any wave can leave
-  }
+  // progress balancing: see balance_step
+  const bool fair = balance_enabled(p);
+  __shared__ int progress[kSWaves];
+  if (fair) balance_init(progress, wave);  // uniform over the workgroup
   if (wave_d0 >= D) return;  // whole wave past the last channel
   const int64_t dtrue = wave_d0 + (lane & 15) + 16 * (lane / (16 * P));
   const bool live = dtrue < D;
@@ -511,18 +527,9 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       }
     }
   };
-  // The balance check runs at the head of each iteration of the time loop
+  // The balance step runs at the head of each iteration of the time loop
   // (every 2 tiles), which is a block boundary anyway, so the unrolled body
   // stays one straight-line block whether or not the launch balances.
-  auto balance = [&](int tile) {
-    __atomic_store_n(&progress[wave], tile, __ATOMIC_RELAXED);
-    const int other = __builtin_amdgcn_readfirstlane(
-        __atomic_load_n(&progress[wave ^ (kWaves / 2)], __ATOMIC_RELAXED));
-    if (tile > other)
-      __builtin_amdgcn_s_setprio(0);
-    else
-      __builtin_amdgcn_s_setprio(1);
-  };
   auto run_tile = [&](const Tile& tb, int tile) {
     stage(tb);
 #pragma unroll
@@ -540,7 +547,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     int tile = 0;
     // Pairs of whole tiles: straight-line code, no per-token guards.
     for (; (tile + 2) * kPF <= nsteps; tile += 2) {
-      if (fair) balance(tile);
+      if (fair) balance_step(progress, wave, tile);
       fetch(t1b, tile + 1);
       run_tile(t0b, tile);
       fetch(t0b, tile + 2);
