@@ -8,7 +8,8 @@ over the whole batch, inputs resident in HBM.  Prints ONE JSON line.
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--extra]
 
 --extra also times the query-time path (top-1 retrieval, state injection,
-32-token query prefill, and its top-3 variant with softmax composition), the
+32-token query prefill; the same with the injection fused into the prefill;
+and its top-3 variant with softmax composition), the
 long-context chunked scan and one layer of the large corpus encode, reported
 under "extra".
 """
@@ -228,6 +229,20 @@ def bench_extra(args):
                       inp["Dskip"], h0, y, hT)
 
     e_ms = time_events(pipeline, 20, flush)
+
+    # the same path with the injection fused into the prefill
+    # (precog_scan_encode_indexed reads store[idx] rows directly)
+    store3 = store.view(cfg["M"], D, N)
+    f_ms = time_events(lambda: P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"],
+                                                     inp["C"], inp["z"], inp["Dskip"], store3,
+                                                     cfg["M"], idx, y, hT), 20, flush)
+
+    def pipeline_fused():
+        P.retrieve_top1(q, K, idx, ws, nws)
+        P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                              inp["Dskip"], store3, cfg["M"], idx, y, hT)
+
+    ef_ms = time_events(pipeline_fused, 20, flush)
     flops = 2.0 * cfg["Q"] * cfg["M"] * cfg["E"]
     sbytes = scan_bytes(wl.batch, wl.seqlen, D, N) + wl.batch * D * N * 2
     res["query_path"] = {
@@ -238,6 +253,8 @@ def bench_extra(args):
         "gather_ms": g_ms, "gather_gbps": 2 * wl.batch * D * N * 2 / (g_ms * 1e-3) / 1e9,
         "prefill_ms": s_ms, "prefill_gbps": sbytes / (s_ms * 1e-3) / 1e9,
         "end_to_end_ms": e_ms,
+        "fused_inject_prefill_ms": f_ms,
+        "end_to_end_fused_ms": ef_ms,
     }
 
     # top-k variant: top-3 retrieval with scores, softmax composition into h0

@@ -150,10 +150,13 @@ size_t precog_scan_workspace_bytes(const precog_scan_desc* desc) {
 
 namespace {
 // precog_scan_encode, and with traj != NULL precog_scan_trajectory.
+// h0_idx non-null: batch row b starts from row h0_idx[b] of the h0_rows-row
+// state store h0 (precog_scan_encode_indexed).
 precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, const float* A,
                    const void* B, const void* C, const void* z, const float* Dskip,
-                   const void* h0, void* y, void* hT, void* traj, int64_t every, void* workspace,
-                   size_t workspace_bytes, void* stream) {
+                   const void* h0, const int32_t* h0_idx, int64_t h0_rows, void* y, void* hT,
+                   void* traj, int64_t every, void* workspace, size_t workspace_bytes,
+                   void* stream) {
   precog_status st = validate_desc(desc);
   if (st != PRECOG_OK) return st;
   const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
@@ -164,7 +167,9 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   if (work && y && !C) return PRECOG_ERR_NULL;
   const int64_t traj_count = traj ? L / every : 0;
   if (!y && !hT && traj_count == 0) return PRECOG_OK;  // nothing requested
-  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, y, hT, workspace, traj};
+  if (h0_idx && h0_rows < 0) return PRECOG_ERR_SHAPE;
+  if (h0_idx && h0_rows > 0 && !h0) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, h0_idx, y, hT, workspace, traj};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
 
@@ -173,7 +178,7 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   if (nchunks > (1LL << 20)) return PRECOG_ERR_SHAPE;
   const ScanWs ws = scan_ws(desc, nchunks);
   if (ws.total > 0 && (!workspace || workspace_bytes < ws.total)) return PRECOG_ERR_WORKSPACE;
-  // channels per workgroup: 256 lanes, N / 16 lanes per channel when N > 16
+  // channels per workgroup: kBlock lanes, N / 16 lanes per channel when N > 16
   const int64_t lanes_per_channel = N > 16 ? N / 16 : 1;
   const int64_t dblocks = ceil_div(D, kBlock / lanes_per_channel);
   if (dblocks * Bt * nchunks > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
@@ -192,6 +197,8 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   p.A = A;
   p.Dskip = y ? Dskip : nullptr;
   p.h0 = h0;
+  p.h0_idx = h0_idx;
+  p.h0_rows = h0_rows;
   p.y = work ? y : nullptr;
   p.hT = hT;
   p.carry = ws.total ? static_cast<float*>(workspace) : nullptr;
@@ -206,7 +213,7 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   p.nchunks = static_cast<int>(nchunks);
   p.dblocks = static_cast<int>(dblocks);
   p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
-            (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
+            ((h0 || h0_idx) ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
   // Progress balancing between the two waves of a SIMD pays when every wave
   // of the launch is resident from the start (at most 4 per SIMD); in launches
   // of many rounds it was measured to cost time, so it is left off there.
@@ -234,8 +241,19 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
                                  const float* A, const void* B, const void* C, const void* z,
                                  const float* Dskip, const void* h0, void* y, void* hT,
                                  void* workspace, size_t workspace_bytes, void* stream) {
-  return scan(desc, x, dt, A, B, C, z, Dskip, h0, y, hT, nullptr, 1, workspace, workspace_bytes,
-              stream);
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, nullptr, 0, y, hT, nullptr, 1, workspace,
+              workspace_bytes, stream);
+}
+
+precog_status precog_scan_encode_indexed(const precog_scan_desc* desc, const void* x,
+                                         const void* dt, const float* A, const void* B,
+                                         const void* C, const void* z, const float* Dskip,
+                                         const void* store, int64_t store_rows,
+                                         const int32_t* h0_idx, void* y, void* hT,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!h0_idx && desc && desc->batch > 0 && desc->dim > 0) return PRECOG_ERR_NULL;
+  return scan(desc, x, dt, A, B, C, z, Dskip, store, h0_idx, store_rows, y, hT, nullptr, 1,
+              workspace, workspace_bytes, stream);
 }
 
 precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x, const void* dt,
@@ -246,7 +264,7 @@ precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x
   if (every < 1) return PRECOG_ERR_SHAPE;
   // traj may be NULL only when nothing would be captured (L < every)
   if (!traj && desc && desc->seqlen >= every) return PRECOG_ERR_NULL;
-  return scan(desc, x, dt, A, B, C, z, Dskip, h0, y, hT, traj, every, workspace,
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, nullptr, 0, y, hT, traj, every, workspace,
               workspace_bytes, stream);
 }
 

@@ -30,6 +30,8 @@ struct ScanParams {
   const float* A_im;  // imaginary part of A (complex-A launches only)
   const float* Dskip;
   const void* h0;
+  const int32_t* h0_idx;  // non-null: batch row b starts from h0 row h0_idx[b] (a state store)
+  int64_t h0_rows;        // rows of that store; an index outside [0, h0_rows) gives a NaN state
   void* y;
   void* hT;
   float* carry;   // [B, C, D, N] fp32: slot 0 = h0, slot c = state entering chunk c

@@ -169,6 +169,19 @@ __device__ __forceinline__ void load_state(float (&h)[N], const float* src) {
   }
 }
 
+// Row of the initial state of batch row b: h0 + b * stride, or, with an
+// index (the injection h_init <- store[idx] fused into the scan),
+// h0 + h0_idx[b] * stride; null when that index is outside the store.
+template <typename TSt>
+__device__ __forceinline__ const TSt* h0_row(const ScanParams& p, int64_t b) {
+  int64_t row = b;
+  if (p.h0_idx != nullptr) {
+    row = p.h0_idx[b];
+    if (row < 0 || row >= p.h0_rows) return nullptr;
+  }
+  return static_cast<const TSt*>(p.h0) + row * p.h0_stride;
+}
+
 template <int N, typename TSt>
 __device__ __forceinline__ void store_state(TSt* dst, const float (&h)[N]) {
 #pragma unroll
@@ -366,7 +379,13 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     if (p.nchunks > 1) {
       load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
     } else if (p.flags & kHasH0) {
-      load_state<NL>(h, static_cast<const TSt*>(p.h0) + b * p.h0_stride + sofs);
+      const TSt* src = h0_row<TSt>(p, b);
+      if (src != nullptr) {
+        load_state<NL>(h, src + sofs);
+      } else {
+#pragma unroll
+        for (int n = 0; n < NL; ++n) h[n] = __builtin_nanf("");
+      }
     } else {
 #pragma unroll
       for (int n = 0; n < NL; ++n) h[n] = 0.f;
@@ -581,7 +600,11 @@ __global__ __launch_bounds__(256) void carry_kernel(const ScanParams p, int N) {
   const int64_t dn = gid - b * DN;
   const int64_t d = dn / N;
   const float a2 = -kLog2e * p.A[dn];
-  float H = (p.flags & kHasH0) ? to_f32(static_cast<const TSt*>(p.h0)[b * p.h0_stride + dn]) : 0.f;
+  float H = 0.f;
+  if (p.flags & kHasH0) {
+    const TSt* src = h0_row<TSt>(p, b);
+    H = src != nullptr ? to_f32(src[dn]) : __builtin_nanf("");
+  }
   float* cp = p.carry + b * p.nchunks * DN + dn;
   const float* sp = p.dtsum + b * p.nchunks * p.D + d;
   cp[0] = H;

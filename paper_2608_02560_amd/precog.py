@@ -24,7 +24,8 @@ STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECO
           4: "PRECOG_ERR_STRIDE", 5: "PRECOG_ERR_ALIGN", 6: "PRECOG_ERR_WORKSPACE",
           7: "PRECOG_ERR_ARCH", 8: "PRECOG_ERR_HIP"}
 
-EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_trajectory",
+EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_encode_indexed",
+           "precog_scan_trajectory",
            "precog_scan_complex",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
            "precog_retrieve_topk", "precog_inject_gather", "precog_inject_compose",
@@ -63,6 +64,9 @@ def lib():
         L.precog_scan_workspace_bytes.restype = sz
         L.precog_scan_encode.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + [sz, vp]
         L.precog_scan_encode.restype = ctypes.c_int
+        L.precog_scan_encode_indexed.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 8 + \
+            [i64, vp, vp, vp, vp, sz, vp]
+        L.precog_scan_encode_indexed.restype = ctypes.c_int
         L.precog_scan_trajectory.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + \
             [i64, vp, sz, vp]
         L.precog_scan_trajectory.restype = ctypes.c_int
@@ -133,6 +137,17 @@ def scan_encode(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None
                                   _ptr(C), _ptr(z), _ptr(Dskip), _ptr(h0), _ptr(y), _ptr(hT),
                                   _ptr(workspace), int(workspace_bytes), _stream(stream))
     _check("precog_scan_encode", st)
+
+
+def scan_encode_indexed(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, store=None,
+                        store_rows=0, h0_idx=None, y=None, hT=None, workspace=None,
+                        workspace_bytes=0, stream=None):
+    """precog_scan_encode_indexed on device tensors (or raw device pointers)."""
+    st = lib().precog_scan_encode_indexed(ctypes.byref(desc), _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
+                                          _ptr(C), _ptr(z), _ptr(Dskip), _ptr(store),
+                                          int(store_rows), _ptr(h0_idx), _ptr(y), _ptr(hT),
+                                          _ptr(workspace), int(workspace_bytes), _stream(stream))
+    _check("precog_scan_encode_indexed", st)
 
 
 def scan_trajectory(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None, y=None,
@@ -233,6 +248,23 @@ def scan(x, dt, A, B, C=None, z=None, Dskip=None, h0=None, *, out_dtype=torch.fl
     scan_encode(desc, x, dt, A, B, C, z, Dskip, h0, y, hT if want_hT else None, ws, nbytes,
                 stream)
     return y, (hT if want_hT else None)
+
+
+def scan_from_store(x, dt, A, B, store, idx, C=None, z=None, Dskip=None, *,
+                    out_dtype=torch.float32, want_y=True, want_hT=True, chunk=0, stream=None):
+    """Runs the scan with batch row b starting from store[idx[b]] (store
+    [M, D, N] in the state dtype, idx [B] int32); returns (y, hT)."""
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    state_dtype = store.dtype
+    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[state_dtype], 0, 0, chunk)
+    y = torch.empty((Bt, L, D), dtype=out_dtype, device=x.device) if want_y else None
+    hT = torch.empty((Bt, D, N), dtype=state_dtype, device=x.device) if want_hT else None
+    nbytes = scan_workspace_bytes(desc)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    scan_encode_indexed(desc, x, dt, A, B, C, z, Dskip, store, store.shape[0], idx, y, hT, ws,
+                        nbytes, stream)
+    return y, hT
 
 
 def trajectory(x, dt, A, B, every, C=None, z=None, Dskip=None, h0=None, *,

@@ -43,6 +43,24 @@ def _encode(desc, x=FAKE, dt=FAKE, A=FAKE, B=FAKE, C=FAKE, z=FAKE, Dskip=FAKE, h
     return P.lib().precog_scan_encode(d, x, dt, A, B, C, z, Dskip, h0, y, hT, ws, wsb, None)
 
 
+def _encode_indexed(desc, store=FAKE, rows=4, idx=FAKE, x=FAKE, y=FAKE, hT=FAKE):
+    d = desc if desc is None else ctypes.byref(desc)
+    return P.lib().precog_scan_encode_indexed(d, x, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, store,
+                                              rows, idx, y, hT, None, 0, None)
+
+
+def test_indexed_scan_validation_errors():
+    good = P.scan_desc(2, 16, 64, 16)
+    assert _encode_indexed(None) == ENULL
+    assert _encode_indexed(good, idx=None) == ENULL           # the index is the point
+    assert _encode_indexed(good, rows=-1) == ESHAPE
+    assert _encode_indexed(good, store=None) == ENULL         # rows > 0 need a store
+    assert _encode_indexed(good, idx=FAKE + 4) == EALIGN
+    assert _encode_indexed(good, store=FAKE + 8) == EALIGN
+    assert _encode_indexed(P.scan_desc(2, 16, 64, 16, h0_batch_stride=64 * 16 - 8)) == ESTRIDE
+    assert _encode_indexed(P.scan_desc(0, 16, 64, 16), idx=None) == OK  # nothing to compute
+
+
 def test_scan_validation_errors():
     good = P.scan_desc(2, 16, 64, 16)
     assert _encode(None) == ENULL

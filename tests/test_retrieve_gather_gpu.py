@@ -140,3 +140,56 @@ def test_gather_more_queries_than_one_grid_dimension():
     torch.cuda.synchronize()
     ref = oracle.gather(store.cpu(), idx.cpu().numpy())
     assert np.array_equal(h0.double().cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("sd", [torch.float16, torch.float32])
+@pytest.mark.parametrize("chunk", [0, 64])
+def test_scan_from_store_equals_gather_then_scan(sd, chunk):
+    """precog_scan_encode_indexed: batch row b starts from store[idx[b]].
+    The injection is fused into the prefill, so y and hT are bitwise those of
+    precog_inject_gather followed by precog_scan_encode (one pass and
+    chunked); an index outside the store starts its row from NaN, as the
+    gather writes NaN for it.  Valid rows also match the oracle."""
+    B, L, D, N, M = 6, 300, 256, 16, 40
+    inp = synth.scan_inputs_host(B, L, D, N, seed=71, in_dtype=torch.bfloat16)
+    d = {k: v.to(DEV) for k, v in inp.items()}
+    store = torch.from_numpy(np.random.default_rng(8).normal(0, 0.5, (M, D, N))).to(sd).to(DEV)
+    idx = torch.tensor([3, 39, -1, 0, 40, 3], dtype=torch.int32, device=DEV)
+    y, hT = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx, d["C"], d["z"],
+                              d["Dskip"], chunk=chunk)
+    h0 = P.gather(store.view(M, D * N), idx, out_dtype=sd).view(B, D, N)
+    y2, h2 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0,
+                    state_dtype=sd, chunk=chunk)
+    torch.cuda.synchronize()
+    ok = torch.tensor([True, True, False, True, False, True])
+    assert torch.equal(y[ok], y2[ok]) and torch.equal(hT[ok], h2[ok])
+    assert torch.isnan(y[~ok]).all() and torch.isnan(hT[~ok]).all()
+    rows = [0, 1, 3, 5]
+    h0_ref = store.double().cpu().numpy()[idx.cpu().numpy()[rows]]
+    sub = {k: (v[rows] if v.dim() == 3 else v) for k, v in inp.items()}
+    y_ref, h_ref = oracle.scan(sub["x"], sub["dt"], sub["A"], sub["B"], sub["C"], sub["z"],
+                               sub["Dskip"], h0_ref, nthreads=8)
+    assert err_rms(y[rows].double().cpu().numpy(), y_ref) <= TOL_BF16
+    assert err_rms(hT[rows].double().cpu().numpy(), h_ref) <= TOL_BF16
+
+
+def test_scan_from_store_query_workload():
+    """The fused query path on the query-time workload: retrieve the top-1
+    state of 256 queries, then prefill 32 tokens starting from store[idx]
+    directly; bitwise equal to gather + scan."""
+    cfg = synth.RETRIEVAL
+    wl = synth.QUERY_PREFILL
+    D, N = wl.dim, wl.dstate
+    q, K, pos, rows = synth.retrieval_inputs_host(cfg["Q"], cfg["M"], cfg["E"], cfg["planted"],
+                                                  cfg["seed"])
+    store = synth.state_store(cfg["M"], D * N, seed=33, device=DEV)
+    inp = synth.scan_inputs_host(wl.batch, wl.seqlen, D, N, wl.seed, torch.bfloat16)
+    d = {k: v.to(DEV) for k, v in inp.items()}
+    idx = P.top1(q.to(DEV), K.to(DEV))
+    y, hT = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store.view(cfg["M"], D, N), idx,
+                              d["C"], d["z"], d["Dskip"], out_dtype=torch.bfloat16)
+    h0 = P.gather(store, idx, out_dtype=torch.float16).view(wl.batch, D, N)
+    y2, h2 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0,
+                    out_dtype=torch.bfloat16, state_dtype=torch.float16)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2) and torch.equal(hT, h2)
