@@ -13,7 +13,8 @@
  *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
  * with the injection fused into the query prefill:
- *   precog_scan_encode_indexed  the scan starting from store[idx] rows
+ *   precog_scan_encode_indexed  the scan starting from store[idx] rows or
+ *                           their top-k softmax composition
  * the SMC trajectory variant of the scan and the complex-A scan:
  *   precog_scan_trajectory  the scan keeping every k-th state (Sec. 5.1-5.2)
  *   precog_scan_complex     Eq. 1 with a diagonal complex A (Sec. 3)
@@ -128,10 +129,14 @@ precog_status precog_scan_encode(const precog_scan_desc *desc, const void *x,
                                  size_t workspace_bytes, void *stream);
 
 /* precog_scan_encode whose initial states come straight from a state store:
- * the query-time injection h_init <- store[idx] (Sec. 4.2) fused into the
- * prefill, so the gathered states are never written out and read back.
+ * the query-time injection (Sec. 4.2) fused into the prefill, so the
+ * injected states are never written out and read back.
  *
- *   h0 of batch row b = store row h0_idx[b]
+ *   h0 of batch row b = store row h0_idx[b]                    (h0_score NULL)
+ *   h0 of batch row b = sum_j w_j store[h0_idx[b*k + j]]       (h0_score given)
+ *
+ * the second with w = softmax(h0_score[b*k .. b*k+k-1] / tau), exactly as
+ * precog_inject_compose forms it (Sec. 5.4 Eq. smc-fusion).
  *
  * Arguments as precog_scan_encode, with h0 replaced by:
  *   store       state rows in desc->state_dtype, row r at store + r*stride
@@ -139,18 +144,25 @@ precog_status precog_scan_encode(const precog_scan_desc *desc, const void *x,
  *               a layer of a multi-layer store is addressed by offsetting
  *               `store` and setting the stride to the row pitch.
  *   store_rows  rows of the store (>= 0).
- *   h0_idx      [B] int32, device memory, 16-byte aligned.  An index outside
- *               [0, store_rows) reads nothing and starts that batch row from
- *               NaN (as precog_inject_gather writes NaN for it).
- * The arithmetic is exactly that of precog_inject_gather into a state of
- * desc->state_dtype followed by precog_scan_encode: the results are bitwise
- * those of the two calls.  hT must not overlap the store.  NULL h0_idx with
- * work to do is PRECOG_ERR_NULL; store may be NULL only when store_rows is 0. */
+ *   h0_idx      [B, k] int32, device memory, 16-byte aligned.  An index
+ *               outside [0, store_rows) reads nothing and starts that batch
+ *               row from NaN (as the gather and the composition write NaN).
+ *   h0_score    [B, k] fp64 retrieval scores (precog_retrieve_topk), 16-byte
+ *               aligned, or NULL for the plain gather (then k must be 1).
+ *   k, tau      rows composed per batch row, 1..64, and the softmax
+ *               temperature, tau > 0 (unused without scores).
+ * The arithmetic is exactly that of precog_inject_gather (or
+ * precog_inject_compose) into a state of desc->state_dtype followed by
+ * precog_scan_encode: the results are bitwise those of the two calls.  hT
+ * must not overlap the store.  NULL h0_idx with work to do is
+ * PRECOG_ERR_NULL; store may be NULL only when store_rows is 0; k or tau out
+ * of range is PRECOG_ERR_SHAPE. */
 precog_status precog_scan_encode_indexed(const precog_scan_desc *desc, const void *x,
                                          const void *dt, const float *A, const void *B,
                                          const void *C, const void *z,
                                          const float *Dskip, const void *store,
                                          int64_t store_rows, const int32_t *h0_idx,
+                                         const double *h0_score, int64_t k, double tau,
                                          void *y, void *hT, void *workspace,
                                          size_t workspace_bytes, void *stream);
 

@@ -6,6 +6,7 @@
 // fp32) so every wave access is a contiguous 1-2 KiB segment.  fp16 -> fp32
 // widening is exact; fp32 -> fp16 rounds to nearest even.  An index outside
 // [0, M) reads nothing and writes NaN.
+#include "compose.h"
 #include "precog_kernels.h"
 
 namespace precog {
@@ -70,10 +71,10 @@ __global__ __launch_bounds__(kBlock) void gather_raw_kernel(const GatherParams p
 }
 
 // Composition: wave 0 of each workgroup turns the k scores of its query into
-// weights w_j = exp((s_j - max s) / tau) / sum_i exp((s_i - max s) / tau) in
-// fp64, rounded once to fp32; then every lane sums w_j h_j in fp32 in rank
-// order (j = 0 first), one fma per term.  k = 1 gives w = 1 exactly, so the
-// result equals the plain gather bit for bit.
+// fp32 weights (compose.h: fp64 softmax, sum in rank order, rounded once);
+// then every lane sums w_j h_j in fp32 in rank order (j = 0 first), one fma
+// per term.  k = 1 gives w = 1 exactly, so the result equals the plain
+// gather bit for bit.
 template <typename TS, typename TO>
 __global__ __launch_bounds__(kBlock) void compose_kernel(const ComposeParams p) {
   const int64_t q = blockIdx.y;
@@ -84,27 +85,13 @@ __global__ __launch_bounds__(kBlock) void compose_kernel(const ComposeParams p) 
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     const bool on = lane < k;
-    const double sj = on ? p.score[q * k + lane] : -INFINITY;
+    const double* srow = p.score + q * k;
+    const SoftmaxDen den = softmax_den(srow, k, p.inv_tau);
     const int32_t ij = on ? p.idx[q * k + lane] : 0;
-    double mx = sj;
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-      const int lo = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2loint(mx)));
-      const int hi = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2hiint(mx)));
-      mx = fmax(mx, __hiloint2double(hi, lo));
-    }
-    const double ej = on ? exp((sj - mx) * p.inv_tau) : 0.0;
-    double tot = ej;
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) {
-      const int lo = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2loint(tot)));
-      const int hi = __builtin_amdgcn_ds_bpermute((lane ^ m) * 4, static_cast<int>(__double2hiint(tot)));
-      tot += __hiloint2double(hi, lo);
-    }
     const bool oob = on && (ij < 0 || ij >= p.M);
     const uint64_t badmask = __ballot(oob);
     if (on) {
-      w[lane] = static_cast<float>(ej / tot);
+      w[lane] = softmax_weight(srow[lane], den, p.inv_tau);
       src[lane] = ij;
     }
     if (lane == 0) bad = badmask != 0;

@@ -150,13 +150,23 @@ size_t precog_scan_workspace_bytes(const precog_scan_desc* desc) {
 
 namespace {
 // precog_scan_encode, and with traj != NULL precog_scan_trajectory.
-// h0_idx non-null: batch row b starts from row h0_idx[b] of the h0_rows-row
-// state store h0 (precog_scan_encode_indexed).
+// Initial states taken from a state store (precog_scan_encode_indexed): batch
+// row b starts from the h0_rows-row store h0 at row h0_idx[b] (h0_score
+// NULL, k = 1) or from the softmax composition of rows h0_idx[b * k + j].
+struct StoreStart {
+  const int32_t* idx;
+  int64_t rows;
+  const double* score;
+  int64_t k;
+  double tau;
+};
+
 precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, const float* A,
                    const void* B, const void* C, const void* z, const float* Dskip,
-                   const void* h0, const int32_t* h0_idx, int64_t h0_rows, void* y, void* hT,
-                   void* traj, int64_t every, void* workspace, size_t workspace_bytes,
-                   void* stream) {
+                   const void* h0, const StoreStart& from, void* y, void* hT, void* traj,
+                   int64_t every, void* workspace, size_t workspace_bytes, void* stream) {
+  const int32_t* h0_idx = from.idx;
+  const int64_t h0_rows = from.rows;
   precog_status st = validate_desc(desc);
   if (st != PRECOG_OK) return st;
   const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
@@ -168,8 +178,11 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   const int64_t traj_count = traj ? L / every : 0;
   if (!y && !hT && traj_count == 0) return PRECOG_OK;  // nothing requested
   if (h0_idx && h0_rows < 0) return PRECOG_ERR_SHAPE;
+  if (h0_idx && (from.k < 1 || from.k > precog::kMaxTopK || (!from.score && from.k != 1)))
+    return PRECOG_ERR_SHAPE;
+  if (from.score && (!(from.tau > 0.0) || !std::isfinite(from.tau))) return PRECOG_ERR_SHAPE;
   if (h0_idx && h0_rows > 0 && !h0) return PRECOG_ERR_NULL;
-  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, h0_idx, y, hT, workspace, traj};
+  const void* ptrs[] = {x, dt, A, B, C, z, Dskip, h0, h0_idx, from.score, y, hT, workspace, traj};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
 
@@ -199,6 +212,9 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   p.h0 = h0;
   p.h0_idx = h0_idx;
   p.h0_rows = h0_rows;
+  p.h0_score = from.score;
+  p.h0_k = static_cast<int>(from.k);
+  p.h0_inv_tau = from.score ? 1.0 / from.tau : 1.0;
   p.y = work ? y : nullptr;
   p.hT = hT;
   p.carry = ws.total ? static_cast<float*>(workspace) : nullptr;
@@ -241,19 +257,21 @@ precog_status precog_scan_encode(const precog_scan_desc* desc, const void* x, co
                                  const float* A, const void* B, const void* C, const void* z,
                                  const float* Dskip, const void* h0, void* y, void* hT,
                                  void* workspace, size_t workspace_bytes, void* stream) {
-  return scan(desc, x, dt, A, B, C, z, Dskip, h0, nullptr, 0, y, hT, nullptr, 1, workspace,
-              workspace_bytes, stream);
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, StoreStart{nullptr, 0, nullptr, 1, 1.0}, y, hT,
+              nullptr, 1, workspace, workspace_bytes, stream);
 }
 
 precog_status precog_scan_encode_indexed(const precog_scan_desc* desc, const void* x,
                                          const void* dt, const float* A, const void* B,
                                          const void* C, const void* z, const float* Dskip,
                                          const void* store, int64_t store_rows,
-                                         const int32_t* h0_idx, void* y, void* hT,
+                                         const int32_t* h0_idx, const double* h0_score,
+                                         int64_t k, double tau, void* y, void* hT,
                                          void* workspace, size_t workspace_bytes, void* stream) {
   if (!h0_idx && desc && desc->batch > 0 && desc->dim > 0) return PRECOG_ERR_NULL;
-  return scan(desc, x, dt, A, B, C, z, Dskip, store, h0_idx, store_rows, y, hT, nullptr, 1,
-              workspace, workspace_bytes, stream);
+  return scan(desc, x, dt, A, B, C, z, Dskip, store,
+              StoreStart{h0_idx, store_rows, h0_score, k, tau}, y, hT, nullptr, 1, workspace,
+              workspace_bytes, stream);
 }
 
 precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x, const void* dt,
@@ -264,8 +282,8 @@ precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x
   if (every < 1) return PRECOG_ERR_SHAPE;
   // traj may be NULL only when nothing would be captured (L < every)
   if (!traj && desc && desc->seqlen >= every) return PRECOG_ERR_NULL;
-  return scan(desc, x, dt, A, B, C, z, Dskip, h0, nullptr, 0, y, hT, traj, every, workspace,
-              workspace_bytes, stream);
+  return scan(desc, x, dt, A, B, C, z, Dskip, h0, StoreStart{nullptr, 0, nullptr, 1, 1.0}, y, hT,
+              traj, every, workspace, workspace_bytes, stream);
 }
 
 namespace {

@@ -30,8 +30,11 @@ struct ScanParams {
   const float* A_im;  // imaginary part of A (complex-A launches only)
   const float* Dskip;
   const void* h0;
-  const int32_t* h0_idx;  // non-null: batch row b starts from h0 row h0_idx[b] (a state store)
-  int64_t h0_rows;        // rows of that store; an index outside [0, h0_rows) gives a NaN state
+  const int32_t* h0_idx;    // non-null: batch row b starts from store rows h0_idx[b * h0_k + j]
+  int64_t h0_rows;          // rows of that store (h0); an index outside [0, h0_rows) gives NaN
+  const double* h0_score;   // non-null: [B, h0_k] scores, the start is their softmax composition
+  int h0_k;                 // rows composed per batch row (1 without scores)
+  double h0_inv_tau;        // 1 / temperature of that composition
   void* y;
   void* hT;
   float* carry;   // [B, C, D, N] fp32: slot 0 = h0, slot c = state entering chunk c

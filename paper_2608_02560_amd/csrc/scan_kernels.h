@@ -39,6 +39,7 @@
 #include <type_traits>
 #include <utility>
 
+#include "compose.h"
 #include "precog_kernels.h"
 
 namespace precog {
@@ -180,6 +181,40 @@ __device__ __forceinline__ const TSt* h0_row(const ScanParams& p, int64_t b) {
     if (row < 0 || row >= p.h0_rows) return nullptr;
   }
   return static_cast<const TSt*>(p.h0) + row * p.h0_stride;
+}
+
+// Initial state composed from the k store rows of batch row b (the top-k
+// injection fused into the scan): sum_j w_j store[idx_j] with the weights of
+// compose.h, one fp32 fma per row in rank order, rounded to the state dtype
+// as the composition kernel would store it; NaN when any index is outside the
+// store.  These are the composition kernel's operations, so the result is
+// the same bits.  `off` is this thread's first element within a row.
+template <int NL, typename TSt>
+__device__ __forceinline__ void compose_state(float (&h)[NL], const ScanParams& p, int64_t b,
+                                              int64_t off) {
+  const int k = p.h0_k;
+  const int32_t* irow = p.h0_idx + b * k;
+  bool bad = false;
+  for (int j = 0; j < k; ++j) bad |= irow[j] < 0 || irow[j] >= p.h0_rows;
+  if (bad) {
+#pragma unroll
+    for (int n = 0; n < NL; ++n) h[n] = __builtin_nanf("");
+    return;
+  }
+  const double* srow = p.h0_score + b * k;
+  const SoftmaxDen den = softmax_den(srow, k, p.h0_inv_tau);
+  float acc[NL];
+#pragma unroll
+  for (int n = 0; n < NL; ++n) acc[n] = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const float wj = softmax_weight(srow[j], den, p.h0_inv_tau);
+    float v[NL];
+    load_state<NL>(v, static_cast<const TSt*>(p.h0) + irow[j] * p.h0_stride + off);
+#pragma unroll
+    for (int n = 0; n < NL; ++n) acc[n] = fmaf(wj, v[n], acc[n]);
+  }
+#pragma unroll
+  for (int n = 0; n < NL; ++n) h[n] = to_f32(from_f32<TSt>(acc[n]));
 }
 
 template <int N, typename TSt>
@@ -378,6 +413,8 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   } else {
     if (p.nchunks > 1) {
       load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
+    } else if (p.h0_score != nullptr) {
+      compose_state<NL, TSt>(h, p, b, sofs);
     } else if (p.flags & kHasH0) {
       const TSt* src = h0_row<TSt>(p, b);
       if (src != nullptr) {
@@ -601,7 +638,11 @@ __global__ __launch_bounds__(256) void carry_kernel(const ScanParams p, int N) {
   const int64_t d = dn / N;
   const float a2 = -kLog2e * p.A[dn];
   float H = 0.f;
-  if (p.flags & kHasH0) {
+  if (p.h0_score != nullptr) {
+    float hv[1];
+    compose_state<1, TSt>(hv, p, b, dn);
+    H = hv[0];
+  } else if (p.flags & kHasH0) {
     const TSt* src = h0_row<TSt>(p, b);
     H = src != nullptr ? to_f32(src[dn]) : __builtin_nanf("");
   }

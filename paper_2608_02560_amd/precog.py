@@ -65,7 +65,7 @@ def lib():
         L.precog_scan_encode.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + [sz, vp]
         L.precog_scan_encode.restype = ctypes.c_int
         L.precog_scan_encode_indexed.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 8 + \
-            [i64, vp, vp, vp, vp, sz, vp]
+            [i64, vp, vp, i64, ctypes.c_double, vp, vp, vp, sz, vp]
         L.precog_scan_encode_indexed.restype = ctypes.c_int
         L.precog_scan_trajectory.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + \
             [i64, vp, sz, vp]
@@ -141,12 +141,13 @@ def scan_encode(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=None
 
 def scan_encode_indexed(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, store=None,
                         store_rows=0, h0_idx=None, y=None, hT=None, workspace=None,
-                        workspace_bytes=0, stream=None):
+                        workspace_bytes=0, stream=None, h0_score=None, k=1, tau=1.0):
     """precog_scan_encode_indexed on device tensors (or raw device pointers)."""
     st = lib().precog_scan_encode_indexed(ctypes.byref(desc), _ptr(x), _ptr(dt), _ptr(A), _ptr(B),
                                           _ptr(C), _ptr(z), _ptr(Dskip), _ptr(store),
-                                          int(store_rows), _ptr(h0_idx), _ptr(y), _ptr(hT),
-                                          _ptr(workspace), int(workspace_bytes), _stream(stream))
+                                          int(store_rows), _ptr(h0_idx), _ptr(h0_score), int(k),
+                                          float(tau), _ptr(y), _ptr(hT), _ptr(workspace),
+                                          int(workspace_bytes), _stream(stream))
     _check("precog_scan_encode_indexed", st)
 
 
@@ -250,10 +251,12 @@ def scan(x, dt, A, B, C=None, z=None, Dskip=None, h0=None, *, out_dtype=torch.fl
     return y, (hT if want_hT else None)
 
 
-def scan_from_store(x, dt, A, B, store, idx, C=None, z=None, Dskip=None, *,
+def scan_from_store(x, dt, A, B, store, idx, C=None, z=None, Dskip=None, *, score=None, tau=1.0,
                     out_dtype=torch.float32, want_y=True, want_hT=True, chunk=0, stream=None):
     """Runs the scan with batch row b starting from store[idx[b]] (store
-    [M, D, N] in the state dtype, idx [B] int32); returns (y, hT)."""
+    [M, D, N] in the state dtype, idx [B] int32), or, with score [B, k] fp64
+    and idx [B, k], from the softmax composition of those k rows; returns
+    (y, hT)."""
     Bt, L, D = x.shape
     N = A.shape[1]
     state_dtype = store.dtype
@@ -262,8 +265,9 @@ def scan_from_store(x, dt, A, B, store, idx, C=None, z=None, Dskip=None, *,
     hT = torch.empty((Bt, D, N), dtype=state_dtype, device=x.device) if want_hT else None
     nbytes = scan_workspace_bytes(desc)
     ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    k = 1 if score is None else score.shape[1]
     scan_encode_indexed(desc, x, dt, A, B, C, z, Dskip, store, store.shape[0], idx, y, hT, ws,
-                        nbytes, stream)
+                        nbytes, stream, h0_score=score, k=k, tau=tau)
     return y, hT
 
 

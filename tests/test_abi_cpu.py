@@ -43,10 +43,11 @@ def _encode(desc, x=FAKE, dt=FAKE, A=FAKE, B=FAKE, C=FAKE, z=FAKE, Dskip=FAKE, h
     return P.lib().precog_scan_encode(d, x, dt, A, B, C, z, Dskip, h0, y, hT, ws, wsb, None)
 
 
-def _encode_indexed(desc, store=FAKE, rows=4, idx=FAKE, x=FAKE, y=FAKE, hT=FAKE):
+def _encode_indexed(desc, store=FAKE, rows=4, idx=FAKE, x=FAKE, y=FAKE, hT=FAKE, score=None,
+                    k=1, tau=1.0):
     d = desc if desc is None else ctypes.byref(desc)
     return P.lib().precog_scan_encode_indexed(d, x, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, store,
-                                              rows, idx, y, hT, None, 0, None)
+                                              rows, idx, score, k, tau, y, hT, None, 0, None)
 
 
 def test_indexed_scan_validation_errors():
@@ -59,6 +60,12 @@ def test_indexed_scan_validation_errors():
     assert _encode_indexed(good, store=FAKE + 8) == EALIGN
     assert _encode_indexed(P.scan_desc(2, 16, 64, 16, h0_batch_stride=64 * 16 - 8)) == ESTRIDE
     assert _encode_indexed(P.scan_desc(0, 16, 64, 16), idx=None) == OK  # nothing to compute
+    assert _encode_indexed(good, k=2) == ESHAPE                 # k > 1 needs scores
+    assert _encode_indexed(good, score=FAKE, k=0) == ESHAPE
+    assert _encode_indexed(good, score=FAKE, k=65) == ESHAPE
+    assert _encode_indexed(good, score=FAKE, k=3, tau=0.0) == ESHAPE
+    assert _encode_indexed(good, score=FAKE, k=3, tau=float("inf")) == ESHAPE
+    assert _encode_indexed(good, score=FAKE + 8, k=3) == EALIGN
 
 
 def test_scan_validation_errors():

@@ -184,3 +184,47 @@ def test_compose_more_queries_than_one_grid_dimension():
     ref = oracle.topk_compose(store.cpu(), idx_n[-500:], sc_n[-500:], 0.5)
     bound = _compose_bound(store.double().cpu().numpy(), idx_n[-500:], sc_n[-500:], 0.5)
     assert np.all(np.abs(h0[-500:].double().cpu().numpy() - ref) <= bound)
+
+
+@pytest.mark.parametrize("sd", [torch.float16, torch.float32])
+@pytest.mark.parametrize("chunk", [0, 64])
+def test_scan_from_composed_store_equals_compose_then_scan(sd, chunk):
+    """precog_scan_encode_indexed with scores: batch row b starts from the
+    softmax composition of its k store rows.  The weights and the fp32 sum
+    are the composition kernel's, and the composed state is rounded to the
+    state dtype as that kernel stores it, so y and hT are bitwise those of
+    precog_inject_compose followed by precog_scan_encode (one pass and
+    chunked).  A row with an index outside the store starts from NaN."""
+    B, L, D, N, M, k = 5, 300, 256, 16, 40, 3
+    inp = synth.scan_inputs_host(B, L, D, N, seed=75, in_dtype=torch.bfloat16)
+    d = {key: v.to(DEV) for key, v in inp.items()}
+    store = torch.from_numpy(np.random.default_rng(9).normal(0, 0.5, (M, D, N))).to(sd).to(DEV)
+    idx = torch.tensor([[3, 39, 0], [7, 7, 1], [5, -1, 2], [0, 1, 2], [9, 40, 8]],
+                       dtype=torch.int32, device=DEV)
+    sc = torch.from_numpy(np.random.default_rng(10).normal(0.2, 0.05, (B, k))).to(DEV)
+    y, hT = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx, d["C"], d["z"],
+                              d["Dskip"], score=sc, tau=0.1, chunk=chunk)
+    h0 = P.compose(store.view(M, D * N), idx, sc, tau=0.1, out_dtype=sd).view(B, D, N)
+    y2, h2 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0,
+                    state_dtype=sd, chunk=chunk)
+    torch.cuda.synchronize()
+    ok = torch.tensor([True, True, False, True, False])
+    assert torch.equal(y[ok], y2[ok]) and torch.equal(hT[ok], h2[ok])
+    assert torch.isnan(y[~ok]).all() and torch.isnan(hT[~ok]).all()
+
+
+def test_scan_from_store_k1_scores_equal_plain_index():
+    """k = 1 with a score: the weight is exactly 1, so the start is the row
+    itself, as without scores."""
+    B, L, D, N, M = 3, 40, 64, 16, 10
+    inp = synth.scan_inputs_host(B, L, D, N, seed=76, in_dtype=torch.float32)
+    d = {key: v.to(DEV) for key, v in inp.items()}
+    store = torch.from_numpy(np.random.default_rng(11).normal(0, 0.5, (M, D, N))).float().to(DEV)
+    idx = torch.tensor([[4], [0], [9]], dtype=torch.int32, device=DEV)
+    sc = torch.tensor([[0.7], [-3.0], [12.0]], dtype=torch.float64, device=DEV)
+    y, hT = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx, d["C"], d["z"],
+                              d["Dskip"], score=sc, tau=0.01)
+    y2, h2 = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx[:, 0].contiguous(),
+                               d["C"], d["z"], d["Dskip"])
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2) and torch.equal(hT, h2)
