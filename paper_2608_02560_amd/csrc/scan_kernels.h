@@ -217,6 +217,52 @@ __device__ __forceinline__ void compose_state(float (&h)[NL], const ScanParams& 
   for (int n = 0; n < NL; ++n) h[n] = to_f32(from_f32<TSt>(acc[n]));
 }
 
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(__double2loint(v)), lane);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(__double2hiint(v)), lane);
+  return __hiloint2double(hi, lo);
+}
+
+// compose_state for a whole wave whose lanes share batch row b (the scan
+// kernel): lane i < k forms exp((s_i - m) / tau) once and the others read it
+// back, the denominator is summed in rank order from those values, and every
+// lane forms w_j = e_j / den: the operations of compose.h, so the same bits,
+// without every lane evaluating 2k exponentials.  The k rows' loads are
+// unrolled so several are in flight.  Every lane of the wave must call it.
+template <int NL, typename TSt>
+__device__ __forceinline__ void compose_state_wave(float (&h)[NL], const ScanParams& p, int64_t b,
+                                                   int64_t off) {
+  const int k = p.h0_k;
+  const int lane = threadIdx.x & 63;
+  const bool on = lane < k;
+  const double si = on ? p.h0_score[b * k + lane] : -INFINITY;
+  const int32_t ii = on ? p.h0_idx[b * k + lane] : 0;
+  if (__ballot(on && (ii < 0 || ii >= p.h0_rows)) != 0) {
+#pragma unroll
+    for (int n = 0; n < NL; ++n) h[n] = __builtin_nanf("");
+    return;
+  }
+  double mx = readlane_f64(si, 0);
+  for (int i = 1; i < k; ++i) mx = fmax(mx, readlane_f64(si, i));
+  const double ei = on ? exp((si - mx) * p.h0_inv_tau) : 0.0;
+  double den = 0.0;
+  for (int i = 0; i < k; ++i) den += readlane_f64(ei, i);
+  float acc[NL];
+#pragma unroll
+  for (int n = 0; n < NL; ++n) acc[n] = 0.f;
+#pragma unroll 4
+  for (int j = 0; j < k; ++j) {
+    const float wj = static_cast<float>(readlane_f64(ei, j) / den);
+    const int64_t row = __builtin_amdgcn_readlane(ii, j);
+    float v[NL];
+    load_state<NL>(v, static_cast<const TSt*>(p.h0) + row * p.h0_stride + off);
+#pragma unroll
+    for (int n = 0; n < NL; ++n) acc[n] = fmaf(wj, v[n], acc[n]);
+  }
+#pragma unroll
+  for (int n = 0; n < NL; ++n) h[n] = to_f32(from_f32<TSt>(acc[n]));
+}
+
 template <int N, typename TSt>
 __device__ __forceinline__ void store_state(TSt* dst, const float (&h)[N]) {
 #pragma unroll
@@ -414,7 +460,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     if (p.nchunks > 1) {
       load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
     } else if (p.h0_score != nullptr) {
-      compose_state<NL, TSt>(h, p, b, sofs);
+      compose_state_wave<NL, TSt>(h, p, b, sofs);
     } else if (p.flags & kHasH0) {
       const TSt* src = h0_row<TSt>(p, b);
       if (src != nullptr) {
