@@ -224,12 +224,14 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E);
  * over the M key rows, the cosine similarity for unit-norm rows.  The result
  * is exact: it equals the argmax of the fp64 inner products summed in index
  * order (products of fp32 values are exact in fp64), ties going to the
- * lowest row.  A matrix-core screen (queries and keys split into bf16
- * high and low parts, three exact products summed in fp32) proposes
- * candidates within a proven error margin and only those are rescored in
- * fp64.  Non-finite inputs give unspecified indices.
+ * lowest row.  A matrix-core screen (queries and keys rounded to
+ * fp16(2^8 v), exact products summed in fp32) proposes candidates within a
+ * proven error margin and only those are rescored in fp64.  Non-finite
+ * inputs give unspecified indices.
  *   query_emb  [Q, E] fp32     index_emb [M, E] fp32 (rows of any norm;
- *              the margin scales with the row norms)
+ *              the margin scales with the row norms; a query or key of norm
+ *              245 or more could overflow the fp16 operands, and then every
+ *              key is rescored: exact, but as slow as a full fp64 search)
  *   idx        [Q] int32 output; M == 0 gives -1
  *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
  *   workspace  precog_retrieve_workspace_bytes(Q, M, E) bytes, 16-byte

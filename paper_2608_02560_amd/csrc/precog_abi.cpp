@@ -287,23 +287,23 @@ precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x
 }
 
 namespace {
-// Retrieval workspace: split queries (2 x [nqg, nks, 64] x 16 B), screen
+// Retrieval workspace: query operands ([nqg, nks, 64] x 16 B), screen
 // scores [Q, 32 nkb], block maxima [Q, nkb], key norms [M] and block norms
 // [nkb], each 256-byte aligned.
 struct RetrieveWs {
-  size_t qsplit, scores, blockmax, rownorm, blocknorm, total;
+  size_t qop, scores, blockmax, rownorm, blocknorm, total;
 };
 RetrieveWs retrieve_ws(int64_t Q, int64_t M, int64_t E) {
   RetrieveWs w;
   const size_t nkb = static_cast<size_t>((M + 31) / 32);
   const size_t nqg = static_cast<size_t>((Q + 127) / 128) * 4;
   const size_t nks = static_cast<size_t>((E + 15) / 16);
-  w.qsplit = align_up(nqg * nks * 64 * 16);
+  w.qop = align_up(nqg * nks * 64 * 16);
   w.scores = align_up(static_cast<size_t>(Q) * nkb * 32 * 4);
   w.blockmax = align_up(static_cast<size_t>(Q) * nkb * 4);
   w.rownorm = align_up(static_cast<size_t>(M) * 4);
   w.blocknorm = align_up(nkb * 4);
-  w.total = 2 * w.qsplit + w.scores + w.blockmax + w.rownorm + w.blocknorm;
+  w.total = w.qop + w.scores + w.blockmax + w.rownorm + w.blocknorm;
   return w;
 }
 }  // namespace
@@ -339,9 +339,8 @@ precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q
   p.q = query_emb;
   p.K = index_emb;
   if (M > 0) {
-    p.qhi = ws;
-    p.qlo = ws + w.qsplit;
-    char* at = ws + 2 * w.qsplit;
+    p.qop = ws;
+    char* at = ws + w.qop;
     p.scores = reinterpret_cast<float*>(at);
     at += w.scores;
     p.blockmax = reinterpret_cast<float*>(at);

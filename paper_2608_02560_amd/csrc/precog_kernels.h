@@ -70,8 +70,7 @@ hipError_t launch_scan_complex(const ScanParams& p, int N, int in_dtype, int out
 struct RetrieveParams {
   const float* q;      // [Q, E]
   const float* K;      // [M, E]
-  void* qhi;           // query bf16 hi parts in operand order (workspace)
-  void* qlo;           // query bf16 lo parts in operand order (workspace)
+  void* qop;           // fp16(2^8 q) in operand order (workspace)
   float* scores;       // [Q, ld_scores] screen scores (workspace)
   float* blockmax;     // [Q, nkb] max screen score per 32-key block (workspace)
   float* rownorm2;     // [M] squared key norms (workspace)

@@ -4,28 +4,33 @@
 // index order (products of fp32 values are exact in fp64), idx = the lowest i
 // attaining the maximum.  Three kernels reach it exactly:
 //
-//   prep     splits every query value v into hi = bf16(v) and lo = bf16(v - hi)
-//            (round to nearest even; v - hi is exact in fp32) and stores them
-//            in the order the matrix-core operands are consumed, so a wave's
-//            operand load is one contiguous 1 KiB segment.
+//   prep     rounds every query value v to fp16(2^8 v) (round to nearest
+//            even; the power-of-two scale is exact and lifts unit-norm
+//            components clear of the fp16 subnormal range) and stores the
+//            values in the order the matrix-core operands are consumed, so a
+//            wave's operand load is one contiguous 1 KiB segment.
 //   screen   workgroup = 32 keys x 128 queries: the keys are read
-//            row-contiguously, split the same way and staged in LDS; each wave
-//            computes a 32 x 32 tile with v_mfma_f32_32x32x16_bf16, summing
-//            q_hi k_hi + q_hi k_lo + q_lo k_hi in fp32 (each product exact).
-//            It stores every screen score S~_i, the maximum of each
+//            row-contiguously, rounded the same way and staged in LDS; each
+//            wave computes a 32 x 32 tile with v_mfma_f32_32x32x16_f16 (each
+//            product of two fp16 values is exact in fp32) and scales it back
+//            by 2^-16.  It stores every screen score S~_i, the maximum of each
 //            (query, 32-key block), and the squared norm of every key and the
 //            largest one of every block.
 //   decide   one wave per query: m = the largest screen score.  A key can
 //            still be the fp64 maximum only if S~_i + e(i) >= m - e(i0), where
-//            e(i) = g |q| |k_i| + tiny bounds the error of its screen score
-//            (g bounds the split error and the fp32 accumulation of the
-//            screen per unit of sum |q_e k_e|, which Cauchy-Schwarz bounds
-//            by |q| |k_i|; it is inflated for the fp32 norms, rounding inside
-//            the matrix core, and the fp64 rounding of the reference).  Blocks
-//            are tested first with their maxima and norm bounds, then the keys
-//            of surviving blocks one by one; every candidate is scored exactly
-//            in fp64 in index order and the best (score, lowest index) wins,
-//            so the result is exact.
+//            e(i) = g |q| |k_i| + h (|q| + |k_i|) + tiny bounds the error of
+//            its screen score (g bounds the fp16 rounding and the fp32
+//            accumulation, taken at twice its round-to-nearest bound, per
+//            unit of sum |q_e k_e|, which Cauchy-Schwarz bounds by |q| |k_i|;
+//            h bounds values below the fp16 normal range per unit of the
+//            1-norms; both are inflated for the fp32 norms and the fp64
+//            rounding of the reference).  Blocks are tested first with their
+//            maxima and norm bounds, then the keys of surviving blocks; every
+//            candidate is scored exactly in fp64 in index order and the best
+//            (score, lowest index) wins, so the result is exact.  A query or
+//            key of norm 245 or more could leave the fp16 range (2^8 |v| past
+//            65504); then the screen proves nothing and every key is scored
+//            in fp64.
 #include "precog_kernels.h"
 
 namespace precog {
@@ -33,14 +38,18 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
+
+// operands are fp16(kScale v); screen scores come back as kUnscale S
+constexpr float kScale = 256.f;
+constexpr float kUnscale = 1.f / 65536.f;
 
 constexpr int kKB = 32;       // keys per block (screen workgroup, block maxima)
 constexpr int kQW = 32;       // queries per wave (one 32 x 32 tile)
 constexpr int kQWG = 4 * kQW; // queries per workgroup
 // features per chunk: the wave preloads its query operands for a whole chunk
-// (2 x kFC / 16 x 4 VGPRs); 128 leaves room for three waves per SIMD
+// (kFC / 16 x 4 VGPRs)
 #ifndef PRECOG_RET_FC
 #define PRECOG_RET_FC 128
 #endif
@@ -58,10 +67,9 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-__device__ __forceinline__ void split4(const float4& v, bf16x4& hi, bf16x4& lo) {
-  const floatx4 f = {v.x, v.y, v.z, v.w};
-  hi = __builtin_convertvector(f, bf16x4);
-  lo = __builtin_convertvector(f - __builtin_convertvector(hi, floatx4), bf16x4);
+__device__ __forceinline__ halfx4 to_op(const float4& v) {
+  const floatx4 f = {v.x * kScale, v.y * kScale, v.z * kScale, v.w * kScale};
+  return __builtin_convertvector(f, halfx4);
 }
 
 // prep: entry ((g * nks + ks) * 2 + h) * 32 + r holds features
@@ -76,25 +84,23 @@ __global__ __launch_bounds__(256) void prep_kernel(const RetrieveParams p) {
   const int ks = static_cast<int>(gk % p.nks);
   const int64_t g = gk / p.nks;
   const int64_t q = g * 32 + r;
-  bf16x4 hi[2], lo[2];
+  halfx4 o[2];
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const int64_t e = 16 * ks + 8 * h + 4 * c;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (q < p.Q && e < p.E) v = *reinterpret_cast<const float4*>(p.q + q * p.E + e);
-    split4(v, hi[c], lo[c]);
+    o[c] = to_op(v);
   }
-  const bf16x8 h8 = {hi[0][0], hi[0][1], hi[0][2], hi[0][3], hi[1][0], hi[1][1], hi[1][2], hi[1][3]};
-  const bf16x8 l8 = {lo[0][0], lo[0][1], lo[0][2], lo[0][3], lo[1][0], lo[1][1], lo[1][2], lo[1][3]};
-  reinterpret_cast<bf16x8*>(p.qhi)[t] = h8;
-  reinterpret_cast<bf16x8*>(p.qlo)[t] = l8;
+  const halfx8 o8 = {o[0][0], o[0][1], o[0][2], o[0][3], o[1][0], o[1][1], o[1][2], o[1][3]};
+  reinterpret_cast<halfx8*>(p.qop)[t] = o8;
 }
 
 // screen: workgroup (kb, qg) = key block kb (keys 32 kb + 0..31) x queries
 // [128 qg, 128 qg + 128), wave w taking 32 of them.  Per feature chunk the
 // workgroup loads the block's key rows row-contiguously and every wave its
 // query operands, all before the first wait (one memory latency per chunk);
-// the keys are split and stored in LDS in operand order
+// the keys are rounded and stored in LDS in operand order
 // [ks][h][row], the row index XOR-swizzled with (2 ks + h) so both the
 // staging writes and the operand reads hit distinct banks.  MFMA operands:
 // lane l supplies row / column l mod 32 and the 8 features of half
@@ -123,8 +129,7 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
 
   // double-buffered: chunk c is staged in buffer c mod 2, so one barrier per
   // chunk separates the staging of c from the reads of c - 1 and c - 2
-  __shared__ bf16x8 khi[2][kKS][2][32];
-  __shared__ bf16x8 klo[2][kKS][2][32];
+  __shared__ halfx8 kop[2][kKS][2][32];
   __shared__ float nsum[2][kKB];
 
   const int srow_base = (tid >> 2) & 31;  // key row this thread stages
@@ -134,10 +139,9 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
       make_rsrc(p.K + k0 * E, static_cast<uint32_t>(nrows * E * 4));
   const uint32_t krow_off = static_cast<uint32_t>(srow_base * E * 4);
   float n2 = 0.f;                         // its share of that row's squared norm
-  // the wave's 32-query group of split operands: nks entries of 1 KiB
+  // the wave's 32-query group of operands: nks entries of 1 KiB
   const uint32_t gbytes = static_cast<uint32_t>(p.nks) * 1024u;
-  const __amdgpu_buffer_rsrc_t hres = make_rsrc(static_cast<const char*>(p.qhi) + g * gbytes, gbytes);
-  const __amdgpu_buffer_rsrc_t lres = make_rsrc(static_cast<const char*>(p.qlo) + g * gbytes, gbytes);
+  const __amdgpu_buffer_rsrc_t ores = make_rsrc(static_cast<const char*>(p.qop) + g * gbytes, gbytes);
   const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
 
   floatx16 acc;
@@ -161,26 +165,22 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
       const uint32_t off = e < E ? krow_off + static_cast<uint32_t>(e * 4) : kDropOffset;
       kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
     }
-    bf16x8 ah[kKS], al[kKS];
+    halfx8 aq[kKS];
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks) {
       const uint32_t so = (ks0 + ks) * 1024u;
-      ah[ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(hres, lane_off, so, 0));
-      al[ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(lres, lane_off, so, 0));
+      aq[ks] = __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(ores, lane_off, so, 0));
     }
 #pragma unroll
     for (int j = 0; j < kFC / 32; ++j) {
       const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
       const float4 v = kv[j];
       n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
-      bf16x4 hi, lo;
-      split4(v, hi, lo);
       const int ks = c4 >> 2;
       const int h = (c4 >> 1) & 1;
       const int sub = c4 & 1;
       const int srow = srow_base ^ ((2 * ks + h) & 31);
-      reinterpret_cast<bf16x4*>(&khi[buf][ks][h][srow])[sub] = hi;
-      reinterpret_cast<bf16x4*>(&klo[buf][ks][h][srow])[sub] = lo;
+      reinterpret_cast<halfx4*>(&kop[buf][ks][h][srow])[sub] = to_op(v);
     }
     __syncthreads();
     if (active) {
@@ -188,11 +188,7 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
       for (int ks = 0; ks < kKS; ++ks) {
         if (ks < nks) {
           const int srow = r32 ^ ((2 * ks + half) & 31);
-          const bf16x8 bh = khi[buf][ks][half][srow];
-          const bf16x8 bl = klo[buf][ks][half][srow];
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], bh, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[ks], bl, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[ks], bh, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(aq[ks], kop[buf][ks][half][srow], acc, 0, 0, 0);
         }
       }
     }
@@ -203,6 +199,7 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
     float mx[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
+      acc[r] *= kUnscale;
       const int64_t q = qw + 8 * (r >> 2) + 4 * half + (r & 3);
       if (q < p.Q && key_ok) p.scores[q * p.ld_scores + key] = acc[r];
       mx[r] = key_ok ? acc[r] : -INFINITY;
@@ -247,21 +244,18 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
   }
 }
 
-__device__ __forceinline__ bool better(double s, int64_t i, double bs, int64_t bi) {
-  return bi < 0 || s > bs || (s == bs && i < bi);
+// the rank order: larger score first, then lower index
+__device__ __forceinline__ bool ranks_before(double s, int i, double bs, int bi) {
+  return s > bs || (s == bs && i < bi);
 }
 
-constexpr int kMaxE = 4096;
-
-__device__ __forceinline__ double shfl_d(double v, int src_lane) {
-  const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2loint(v)));
-  const int hi = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2hiint(v)));
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(__double2loint(v)), l);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(__double2hiint(v)), l);
   return __hiloint2double(hi, lo);
 }
 
-__device__ __forceinline__ int shfl_i(int v, int src_lane) {
-  return __builtin_amdgcn_ds_bpermute(src_lane * 4, v);
-}
+constexpr int kMaxE = 4096;
 
 // (value, index) order of the block-maximum pass: larger value first, then
 // lower index.  NaN values are never ranked.
@@ -269,7 +263,10 @@ __device__ __forceinline__ bool before(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-constexpr int kCand = 64;             // candidate list capacity (indices)
+constexpr int kCand = 256;            // candidate list capacity (indices)
+// squared norm below which 2^8 |v| stays under the fp16 overflow threshold
+// for every component v (|v| < 245)
+constexpr float kMaxNorm2 = 60000.f;
 constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
 
 // decide: one 64-lane workgroup per query (see the file comment).  For the
@@ -282,9 +279,10 @@ constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
 // pitch E + 4 words, 16-byte aligned)
 // and lane j sums row j in fp64 in feature order (fma equals
 // multiply-then-add here: the product of two fp32 values is exact in fp64),
-// so the chains of a batch run side by side.  Scores enter a rank list
-// spread over the lanes (lane j holds rank j), ordered by score, then by
-// lower index; the order of insertion does not change the list.
+// so the chains of a batch run side by side.  Each scored batch is merged
+// into a rank list spread over the lanes (lane j holds rank j), ordered by
+// score, then by lower index; the order of the batches does not change the
+// list.
 __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const int64_t q = blockIdx.x;
   const int lane = threadIdx.x;
@@ -294,18 +292,32 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   __shared__ __attribute__((aligned(16))) float qs[kMaxE];
   __shared__ __attribute__((aligned(16))) float rs[kRowWords];
   __shared__ int cand[kCand];
+  __shared__ double slot_s[64];
+  __shared__ int slot_i[64];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
   const float* bm = p.blockmax + q * nkb;
   const float* sc = p.scores + q * p.ld_scores;
 
+  // fixed-width groups of predicated loads, so every load of a group is in
+  // flight before the first is consumed
+  const int e4n = E / 4;
   float nq = 0.f;
-#pragma unroll 4
-  for (int e4 = lane; e4 < E / 4; e4 += 64) {
-    const float4 v = qg4[e4];
-    *reinterpret_cast<float4*>(qs + 4 * e4) = v;
-    nq = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, nq))));
+  for (int g0 = 0; g0 < e4n; g0 += 4 * 64) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e4 = g0 + 64 * u + lane;
+      v[u] = e4 < e4n ? qg4[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e4 = g0 + 64 * u + lane;
+      if (e4 < e4n) *reinterpret_cast<float4*>(qs + 4 * e4) = v[u];
+      nq = fmaf(v[u].x, v[u].x, fmaf(v[u].y, v[u].y, fmaf(v[u].z, v[u].z, fmaf(v[u].w, v[u].w, nq))));
+    }
   }
-  const float qnorm = sqrtf(wave_sum(nq));
+  const float qnorm2 = wave_sum(nq);
+  const float qnorm = sqrtf(qnorm2);
 
   // t_k: k rounds, each taking the first (value, index) pair after the
   // previous one (the first round also takes the largest block norm); fewer
@@ -358,57 +370,107 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   for (int s = 1; s < 64; s <<= 1) nmax = fmaxf(nmax, xor_shfl(nmax, s));
   const float tk = found ? tv : -INFINITY;
 
-  // Screen-score error bound per unit of |q| |k_i|: dropped split terms
-  // q_lo k_lo + (q_hi + q_lo) dk + dq k <= 3.05 * 2^-16 (bf16 rounding 2^-8
-  // relative, twice), plus fp32 accumulation of 3E exact products, gamma_3E
-  // (with 1.008 for |hi| + |lo| > |v|); doubled for any rounding the matrix
-  // core performs inside one instruction, the fp32 norms and the fp64
-  // reference's own rounding.
+  // Screen-score error bound.  Each operand value w = fp16(2^8 v) / 2^8
+  // has |w - v| <= a |v| + bs: a = 2^-11 (round to nearest in the fp16
+  // normal range), bs = 2^-22 (below it, whether rounded to a subnormal or
+  // flushed to zero).  So |q~ k~ - q k| <= (2a + a^2) |q k| + bs (1 + a)
+  // (|q| + |k|) + bs^2 per feature; summed with Cauchy-Schwarz for the
+  // products and |v|_1 <= sqrt(E) |v| for the 1-norms.  The fp32 sum of the E
+  // exact products adds at most 2 gamma_E times their absolute sum (twice
+  // the round-to-nearest bound, so additions that truncate, or align the
+  // products of one instruction to the largest, are covered too); the 2^-16
+  // scale back is exact (or below 2^-149).  The factor 1.01 covers the fp32
+  // norms (relative error ~gamma_E) and 1e-12 the fp64 reference's own
+  // rounding.  A norm past kMaxNorm2 could overflow fp16 (2^8 |v| >= 65520):
+  // then every key is scored exactly.
   const double u = 5.9604644775390625e-08;  // 2^-24
-  const double n3 = 3.0 * static_cast<double>(E);
-  const double gam = (n3 * u) / (1.0 - n3 * u);
-  const double g = 2.0 * (1.008 * gam + 3.05 * 1.52587890625e-05) + 1e-12;
-  const double tiny = 1e-30;
-  const double gq = g * static_cast<double>(qnorm);
-  const double thresh = static_cast<double>(tk) - (gq * sqrt(static_cast<double>(nmax)) + tiny);
+  const double a = 4.8828125e-04;           // 2^-11
+  const double bs = 2.384185791015625e-07;  // 2^-22
+  const double en = static_cast<double>(E);
+  const double gam2 = 2.0 * (en * u) / (1.0 - en * u);
+  const double g = 1.01 * (2.0 * a + a * a + gam2 * (1.0 + 2.0 * a + a * a)) + 1e-12;
+  const double h = 1.01 * (1.0 + gam2) * bs * (1.0 + a) * sqrt(en);
+  const double tiny = 1.01 * (1.0 + gam2) * en * bs * bs + 1e-30;
+  const double qn = static_cast<double>(qnorm);
+  const double gq = g * qn + h;
+  const double hq = h * qn + tiny;
+  // error bound of a screen score whose key has squared norm <= n2
+  auto err = [&](float n2) { return gq * sqrt(static_cast<double>(n2)) + hq; };
+  const bool exhaustive = !(qnorm2 < kMaxNorm2) || !(nmax < kMaxNorm2);
+  const double thresh = exhaustive ? -INFINITY : static_cast<double>(tk) - err(nmax);
 
-  // rank list: lane j < k holds the j-th best (score, index) so far
+  // rank list: lane j < nl holds the j-th best (score, index) so far
   double ls = -INFINITY;
-  int64_t li = -1;
-  auto insert = [&](double s, int64_t ii) {
-    const bool ahead = lane < k && li >= 0 && better(ls, li, s, ii);
-    const int pos = __builtin_popcountll(__ballot(ahead));
-    if (pos < k) {
-      const double ps = shfl_d(ls, lane > 0 ? lane - 1 : 0);
-      const int pil = shfl_i(static_cast<int>(li), lane > 0 ? lane - 1 : 0);
-      if (lane > pos) {
-        ls = ps;
-        li = pil;
-      } else if (lane == pos) {
-        ls = s;
-        li = ii;
+  int li = -1;
+  int nl = 0;
+  // merge a scored batch (lane r < nb: score s of key ci) into the list:
+  // every element counts the elements of both sets ordered before it
+  // (broadcast one pair per step), so its new rank is known at once, and
+  // the elements with rank < k go through LDS to the lane of their rank.
+  // Keys are distinct, so ranks are distinct.
+  auto merge = [&](double s, int ci, int nb) {
+    const double sk = s != s ? -INFINITY : s;  // NaN scores rank last
+    int before_new = 0;                        // for this lane's batch element
+    int new_before_old = 0;                    // for this lane's list element
+    const int steps = nl > nb ? nl : nb;
+    for (int i = 0; i < steps; ++i) {
+      if (i < nl) {
+        const double es = readlane_d(ls, i);
+        const int ei = __builtin_amdgcn_readlane(li, i);
+        before_new += (lane < nb && ranks_before(es, ei, sk, ci)) ? 1 : 0;
       }
+      if (i < nb) {
+        const double ns = readlane_d(sk, i);
+        const int ni = __builtin_amdgcn_readlane(ci, i);
+        before_new += (lane < nb && i != lane && ranks_before(ns, ni, sk, ci)) ? 1 : 0;
+        new_before_old += (lane < nl && ranks_before(ns, ni, ls, li)) ? 1 : 0;
+      }
+    }
+    __syncthreads();  // the previous merge has read its slots
+    if (lane < nl && lane + new_before_old < k) {
+      slot_s[lane + new_before_old] = ls;
+      slot_i[lane + new_before_old] = li;
+    }
+    if (lane < nb && before_new < k) {
+      slot_s[before_new] = sk;
+      slot_i[before_new] = ci;
+    }
+    __syncthreads();
+    nl = nl + nb < k ? nl + nb : k;
+    if (lane < nl) {
+      ls = slot_s[lane];
+      li = slot_i[lane];
     }
   };
 
   // exact scores of the listed candidates, a batch of rows at a time
   const int pitch = E + 4;  // E is a multiple of 4: rows stay 16-byte aligned
+  const uint64_t inv_e4n = ((1ull << 32) + static_cast<uint64_t>(e4n) - 1) / static_cast<uint64_t>(e4n);
   const int batch_max = kRowWords / pitch < 64 ? kRowWords / pitch : 64;
   int ncand = 0;
   auto flush = [&]() {
     for (int c0 = 0; c0 < ncand; c0 += batch_max) {
       const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
       __syncthreads();  // previous batch consumed, list and qs complete
-      // one flat (row, float4) space, so the loads of several rows are in
-      // flight together
-      const int e4n = E / 4;
-#pragma unroll 8
-      for (int f = lane; f < nb * e4n; f += 64) {
-        const int r = f / e4n;
-        const int e4 = f - r * e4n;
-        const float4 v =
-            reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4];
-        *reinterpret_cast<float4*>(rs + r * pitch + 4 * e4) = v;
+      // one flat (row, float4) space in fixed-width groups of predicated
+      // loads, so the loads of several rows are in flight together
+      // (f / e4n as a 64-bit multiply-high: exact for f < 2^17, e4n <= 1024)
+      const int tot = nb * e4n;
+      for (int f0 = 0; f0 < tot; f0 += 8 * 64) {
+        float4 v[8];
+        int off[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int f = f0 + 64 * u + lane;
+          const int r = f < tot ? static_cast<int>((static_cast<uint64_t>(f) * inv_e4n) >> 32) : 0;
+          const int e4 = f - r * e4n;
+          off[u] = f < tot ? r * pitch + 4 * e4 : -1;
+          v[u] = f < tot ? reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4]
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (off[u] >= 0) *reinterpret_cast<float4*>(rs + off[u]) = v[u];
       }
       __syncthreads();
       // the chain stays one fma per feature in feature order; reading four
@@ -427,11 +489,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
           s = fma(static_cast<double>(qv.w), static_cast<double>(rv.w), s);
         }
       }
-      for (int r = 0; r < nb; ++r) {
-        const int lo = __builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(__double2loint(s)));
-        const int hi = __builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(__double2hiint(s)));
-        insert(__hiloint2double(hi, lo), cand[c0 + r]);
-      }
+      merge(s, lane < nb ? cand[c0 + lane] : -1, nb);
     }
     ncand = 0;
   };
@@ -446,23 +504,42 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
         b = bm[kb];
         n = p.blocknorm2[kb];
       }
-      const bool pass = kb < nkb && static_cast<double>(b) + gq * sqrt(static_cast<double>(n)) + tiny >= thresh;
+      const bool pass = kb < nkb && (exhaustive || static_cast<double>(b) + err(n) >= thresh);
       bmask[j] = __ballot(pass);
     }
+    // keys of the surviving blocks, eight blocks per round (two per 64-lane
+    // pass) so their score and norm loads are in flight together
+    const int half = lane >> 5;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      while (bmask[j]) {
-        const int blk = kb0 + 64 * j + __builtin_ctzll(bmask[j]);
-        bmask[j] &= bmask[j] - 1;
-        const int64_t i = static_cast<int64_t>(blk) * kKB + (lane & (kKB - 1));
-        bool cand_ok = false;
-        if (lane < kKB && i < p.M)
-          cand_ok = static_cast<double>(sc[i]) + gq * sqrt(static_cast<double>(p.rownorm2[i])) + tiny >= thresh;
-        const uint64_t cmask = __ballot(cand_ok);
-        if (!cmask) continue;
-        if (ncand + kKB > kCand) flush();
-        if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(i);
-        ncand += __builtin_popcountll(cmask);
+      uint64_t m = bmask[j];
+      while (m) {
+        int blk[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          blk[u] = m ? kb0 + 64 * j + __builtin_ctzll(m) : -1;
+          m &= m - 1;
+        }
+        int64_t ii[4];
+        bool ok[4];
+        float sv[4], nv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int b = half ? blk[2 * r + 1] : blk[2 * r];
+          ii[r] = static_cast<int64_t>(b) * kKB + (lane & (kKB - 1));
+          ok[r] = b >= 0 && ii[r] < p.M;
+          sv[r] = ok[r] ? sc[ii[r]] : 0.f;
+          nv[r] = ok[r] ? p.rownorm2[ii[r]] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool cand_ok = ok[r] && (exhaustive || static_cast<double>(sv[r]) + err(nv[r]) >= thresh);
+          const uint64_t cmask = __ballot(cand_ok);
+          if (!cmask) continue;
+          if (ncand + 64 > kCand) flush();
+          if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(ii[r]);
+          ncand += __builtin_popcountll(cmask);
+        }
       }
     }
   }

@@ -33,7 +33,7 @@ def test_retrieval_workload_bit_exact():
 
 
 @pytest.mark.parametrize("Q,M,E", [(1, 1, 4), (3, 33, 16), (65, 1000, 20), (70, 97, 388),
-                                   (130, 4099, 64), (8, 20000, 1024)])
+                                   (130, 4099, 64), (8, 20000, 1024), (5, 70001, 8)])
 def test_retrieval_ragged_shapes(Q, M, E):
     q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 4), seed=Q * 7 + M + E)
     ref, _ = oracle.top1(q, K, nthreads=8)
@@ -71,6 +71,47 @@ def test_retrieval_non_unit_rows_and_empty():
     assert np.array_equal(_gpu_top1(q, K2), ref)
     empty = _gpu_top1(q, K[:0])
     assert np.all(empty == -1)
+
+
+def test_retrieval_norms_past_the_screen_range():
+    """Rows (or a query) whose components could overflow the fp16 screen
+    operands: the screen proves nothing, every key is scored in fp64, and
+    the answer is still the exact one."""
+    q, K, _, _ = synth.retrieval_inputs_host(24, 700, 128, 4, seed=63)
+    K2 = K.clone()
+    K2[::97] *= 1000.0          # norms 1000: 2^8 |v| can pass 65504
+    ref, _ = oracle.top1(q, K2)
+    assert np.array_equal(_gpu_top1(q, K2), ref)
+    q2 = q.clone()
+    q2[5] *= 300.0
+    ref, _ = oracle.top1(q2, K)
+    assert np.array_equal(_gpu_top1(q2, K), ref)
+    # largest norm just inside the range: the screen and its bound hold
+    K3 = K.clone()
+    K3[::50] *= 200.0
+    ref, _ = oracle.top1(q, K3)
+    assert np.array_equal(_gpu_top1(q, K3), ref)
+
+
+def test_retrieval_components_below_fp16_normal_range():
+    """Keys and queries with many components far below 2^-22 (subnormal or
+    zero once scaled into fp16) and near-ties decided by them."""
+    g = np.random.default_rng(64)
+    q, K, _, _ = synth.retrieval_inputs_host(32, 900, 96, 0, seed=64)
+    qn, Kn = q.numpy().copy(), K.numpy().copy()
+    tiny = g.random(Kn.shape) < 0.5
+    Kn[tiny] *= np.float32(1e-7)
+    qn[g.random(qn.shape) < 0.5] *= np.float32(1e-8)
+    win, _ = oracle.top1(qn, Kn)
+    for i, w in enumerate(win[:16]):
+        # a copy of the winner that differs only in components far below the
+        # fp16 screen's resolution
+        near = Kn[w].copy()
+        c = int(g.integers(0, 96))
+        near[c] = np.float32(near[c] + np.sign(qn[i, c]) * 1e-9)
+        Kn[(w + 7) % 900] = near
+    ref, _ = oracle.top1(qn, Kn)
+    assert np.array_equal(_gpu_top1(torch.from_numpy(qn), torch.from_numpy(Kn)), ref)
 
 
 @pytest.mark.parametrize("sd,od", [(torch.float16, torch.float16), (torch.float16, torch.float32),

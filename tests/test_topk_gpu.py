@@ -165,10 +165,10 @@ def test_topk_query_path_end_to_end():
     assert err_rms(hT.double().cpu().numpy(), h_ref) <= TOL_BF16
 
 
-@pytest.mark.parametrize("Q,M,E,k", [(20, 300, 4096, 5), (9, 7, 16, 7)])
+@pytest.mark.parametrize("Q,M,E,k", [(20, 300, 4096, 5), (9, 7, 16, 7), (6, 70001, 8, 3)])
 def test_topk_extreme_shapes(Q, M, E, k):
-    """E = 4096 (one candidate row per rescoring batch) and k = M (every key
-    ranked) on a single partial key block."""
+    """E = 4096 (one candidate row per rescoring batch), k = M (every key
+    ranked) on a single partial key block, and 2,188 key blocks."""
     q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 3), seed=Q * 3 + M + E)
     _check_topk(q, K, k)
 
