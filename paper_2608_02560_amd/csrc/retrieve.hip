@@ -61,10 +61,44 @@ __device__ __forceinline__ float xor_shfl(float v, int m) {
   return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, v)));
 }
 
+// Wave-wide reductions with DPP row operations (no LDS round trips): swap
+// neighbours, swap pairs, rotate the row by 4 then by 8, so every lane holds
+// its 16-lane row's result; the four rows' results are combined from
+// readlanes, so the value is wave-uniform.
+template <int kCtrl>
+__device__ __forceinline__ int dpp(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, kCtrl, 0xf, 0xf, false);
+}
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, dpp<kCtrl>(__builtin_bit_cast(int, v)));
+}
+constexpr int kQuadSwap1 = 0xB1;  // quad_perm [1, 0, 3, 2]
+constexpr int kQuadSwap2 = 0x4E;  // quad_perm [2, 3, 0, 1]
+constexpr int kRowRor4 = 0x124;
+constexpr int kRowRor8 = 0x128;
+
+__device__ __forceinline__ int readlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float readlane(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+  v = op(v, dpp<kQuadSwap1>(v));
+  v = op(v, dpp<kQuadSwap2>(v));
+  v = op(v, dpp<kRowRor4>(v));
+  v = op(v, dpp<kRowRor8>(v));
+  return op(op(readlane(v, 0), readlane(v, 16)), op(readlane(v, 32), readlane(v, 48)));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+}
+__device__ __forceinline__ int wave_min(int v) {
+  return wave_reduce(v, [](int a, int b) { return a < b ? a : b; });
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v += xor_shfl(v, m);
-  return v;
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 
 __device__ __forceinline__ halfx4 to_op(const float4& v) {
@@ -268,6 +302,7 @@ constexpr int kCand = 256;            // candidate list capacity (indices)
 // for every component v (|v| < 245)
 constexpr float kMaxNorm2 = 60000.f;
 constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
+constexpr int kCacheGroups = 2;       // 256-block groups whose maxima stay in registers
 
 // decide: one 64-lane workgroup per query (see the file comment).  For the
 // k best keys the bound uses t_k, the k-th largest block maximum: k distinct
@@ -298,6 +333,20 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const float* bm = p.blockmax + q * nkb;
   const float* sc = p.scores + q * p.ld_scores;
 
+  // the block maxima and norms of the first kCacheGroups x 256 blocks,
+  // loaded once (in flight with the query row) and held in registers for
+  // the t_k rounds and the block tests; blocks past nkb hold NaN / 0
+  float cb[4 * kCacheGroups], cn[4 * kCacheGroups];
+#pragma unroll
+  for (int g = 0; g < kCacheGroups; ++g) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kb = 256 * g + 64 * j + lane;
+      cb[4 * g + j] = kb < nkb ? bm[kb] : __builtin_nanf("");
+      cn[4 * g + j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
+    }
+  }
+
   // fixed-width groups of predicated loads, so every load of a group is in
   // flight before the first is consumed
   const int e4n = E / 4;
@@ -323,6 +372,8 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   // previous one (the first round also takes the largest block norm); fewer
   // than k ranked blocks leave t_k = -inf (every key is then a candidate)
   float nmax = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4 * kCacheGroups; ++c) nmax = fmaxf(nmax, cn[c]);
   float tv = INFINITY;
   int ti = -1;
   bool found = true;
@@ -330,7 +381,16 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     float bv = -INFINITY;
     int bi = 0x7fffffff;
     bool any = false;
-    for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
+    auto consider = [&](float b, int kb) {
+      if (before(tv, ti, b, kb) && (!any || before(b, kb, bv, bi))) {
+        bv = b;
+        bi = kb;
+        any = true;
+      }
+    };
+#pragma unroll
+    for (int c = 0; c < 4 * kCacheGroups; ++c) consider(cb[c], 64 * c + lane);
+    for (int kb0 = 256 * kCacheGroups; kb0 < nkb; kb0 += 256) {
       float b[4], n[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -340,34 +400,21 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int kb = kb0 + 64 * j + lane;
         nmax = fmaxf(nmax, n[j]);
-        if (before(tv, ti, b[j], kb) && (!any || before(b[j], kb, bv, bi))) {
-          bv = b[j];
-          bi = kb;
-          any = true;
-        }
+        consider(b[j], kb0 + 64 * j + lane);
       }
     }
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-      const float ov = xor_shfl(bv, s);
-      const int oi = __builtin_amdgcn_ds_bpermute((lane ^ s) * 4, bi);
-      const bool oany = __builtin_amdgcn_ds_bpermute((lane ^ s) * 4, static_cast<int>(any)) != 0;
-      if (oany && (!any || before(ov, oi, bv, bi))) {
-        bv = ov;
-        bi = oi;
-        any = true;
-      }
-    }
-    found = any;
-    if (any) {
-      tv = bv;
-      ti = bi;
+    // the wave's first pair: the largest value, then the lowest index among
+    // the lanes holding it (lanes without a pair take no part)
+    const float m = wave_max(any ? bv : -INFINITY);
+    const int mi = wave_min(any && bv == m ? bi : 0x7fffffff);
+    found = __ballot(any) != 0;
+    if (found) {
+      tv = m;
+      ti = mi;
     }
   }
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) nmax = fmaxf(nmax, xor_shfl(nmax, s));
+  nmax = wave_max(nmax);
   const float tk = found ? tv : -INFINITY;
 
   // Screen-score error bound.  Each operand value w = fp16(2^8 v) / 2^8
@@ -494,17 +541,14 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     ncand = 0;
   };
 
-  for (int kb0 = 0; kb0 < nkb; kb0 += 256) {
+  // one group of 256 blocks: lane l holds the maxima and norms of blocks
+  // kb0 + 64 j + l
+  auto test_group = [&](int kb0, const float (&b4)[4], const float (&n4)[4]) {
     uint64_t bmask[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kb = kb0 + 64 * j + lane;
-      float b = -INFINITY, n = 0.f;
-      if (kb < nkb) {
-        b = bm[kb];
-        n = p.blocknorm2[kb];
-      }
-      const bool pass = kb < nkb && (exhaustive || static_cast<double>(b) + err(n) >= thresh);
+      const bool pass = kb < nkb && (exhaustive || static_cast<double>(b4[j]) + err(n4[j]) >= thresh);
       bmask[j] = __ballot(pass);
     }
     // keys of the surviving blocks, eight blocks per round (two per 64-lane
@@ -542,6 +586,24 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
         }
       }
     }
+  };
+#pragma unroll
+  for (int g = 0; g < kCacheGroups; ++g) {
+    if (256 * g < nkb) {
+      const float b4[4] = {cb[4 * g], cb[4 * g + 1], cb[4 * g + 2], cb[4 * g + 3]};
+      const float n4[4] = {cn[4 * g], cn[4 * g + 1], cn[4 * g + 2], cn[4 * g + 3]};
+      test_group(256 * g, b4, n4);
+    }
+  }
+  for (int kb0 = 256 * kCacheGroups; kb0 < nkb; kb0 += 256) {
+    float b4[4], n4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kb = kb0 + 64 * j + lane;
+      b4[j] = kb < nkb ? bm[kb] : -INFINITY;
+      n4[j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
+    }
+    test_group(kb0, b4, n4);
   }
   flush();
   if (lane < k) {
