@@ -226,8 +226,10 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E);
  * order (products of fp32 values are exact in fp64), ties going to the
  * lowest row.  A matrix-core screen (queries and keys rounded to
  * fp16(2^8 v), exact products summed in fp32) proposes candidates within a
- * proven error margin and only those are rescored in fp64.  Non-finite
- * inputs give unspecified indices.
+ * proven error margin and only those are rescored in fp64 (a lone candidate
+ * needs none; several are ordered by an fp64 tree sum when its proven error
+ * separates them, else by the sequential fp64 sums).  Non-finite inputs give
+ * unspecified indices.
  *   query_emb  [Q, E] fp32     index_emb [M, E] fp32 (rows of any norm;
  *              the margin scales with the row norms; a query or key of norm
  *              245 or more could overflow the fp16 operands, and then every

@@ -100,6 +100,25 @@ __device__ __forceinline__ int wave_min(int v) {
 __device__ __forceinline__ float wave_sum(float v) {
   return wave_reduce(v, [](float a, float b) { return a + b; });
 }
+// fp64 sum over the wave in the same pattern (the halves move together)
+template <int kCtrl>
+__device__ __forceinline__ double dpp_d(double v) {
+  const int lo = dpp<kCtrl>(static_cast<int>(__double2loint(v)));
+  const int hi = dpp<kCtrl>(static_cast<int>(__double2hiint(v)));
+  return __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(__double2loint(v)), l);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(__double2hiint(v)), l);
+  return __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ double wave_sum_d(double v) {
+  v += dpp_d<kQuadSwap1>(v);
+  v += dpp_d<kQuadSwap2>(v);
+  v += dpp_d<kRowRor4>(v);
+  v += dpp_d<kRowRor8>(v);
+  return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
+}
 
 __device__ __forceinline__ halfx4 to_op(const float4& v) {
   const floatx4 f = {v.x * kScale, v.y * kScale, v.z * kScale, v.w * kScale};
@@ -283,11 +302,6 @@ __device__ __forceinline__ bool ranks_before(double s, int i, double bs, int bi)
   return s > bs || (s == bs && i < bi);
 }
 
-__device__ __forceinline__ double readlane_d(double v, int l) {
-  const int lo = __builtin_amdgcn_readlane(static_cast<int>(__double2loint(v)), l);
-  const int hi = __builtin_amdgcn_readlane(static_cast<int>(__double2hiint(v)), l);
-  return __hiloint2double(hi, lo);
-}
 
 constexpr int kMaxE = 4096;
 
@@ -495,31 +509,36 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const uint64_t inv_e4n = ((1ull << 32) + static_cast<uint64_t>(e4n) - 1) / static_cast<uint64_t>(e4n);
   const int batch_max = kRowWords / pitch < 64 ? kRowWords / pitch : 64;
   int ncand = 0;
+  bool early = false;  // a batch was scored before the list was complete
+  // rows cand[c0 .. c0 + nb) into rs (row pitch `pitch`): one flat
+  // (row, float4) space in fixed-width groups of predicated loads, so the
+  // loads of several rows are in flight together (f / e4n as a 64-bit
+  // multiply-high: exact for f < 2^17, e4n <= 1024)
+  auto stage_rows = [&](int c0, int nb) {
+    __syncthreads();  // previous batch consumed, list and qs complete
+    const int tot = nb * e4n;
+    for (int f0 = 0; f0 < tot; f0 += 8 * 64) {
+      float4 v[8];
+      int off[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int f = f0 + 64 * u + lane;
+        const int r = f < tot ? static_cast<int>((static_cast<uint64_t>(f) * inv_e4n) >> 32) : 0;
+        const int e4 = f - r * e4n;
+        off[u] = f < tot ? r * pitch + 4 * e4 : -1;
+        v[u] = f < tot ? reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4]
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (off[u] >= 0) *reinterpret_cast<float4*>(rs + off[u]) = v[u];
+    }
+    __syncthreads();
+  };
   auto flush = [&]() {
     for (int c0 = 0; c0 < ncand; c0 += batch_max) {
       const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
-      __syncthreads();  // previous batch consumed, list and qs complete
-      // one flat (row, float4) space in fixed-width groups of predicated
-      // loads, so the loads of several rows are in flight together
-      // (f / e4n as a 64-bit multiply-high: exact for f < 2^17, e4n <= 1024)
-      const int tot = nb * e4n;
-      for (int f0 = 0; f0 < tot; f0 += 8 * 64) {
-        float4 v[8];
-        int off[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int f = f0 + 64 * u + lane;
-          const int r = f < tot ? static_cast<int>((static_cast<uint64_t>(f) * inv_e4n) >> 32) : 0;
-          const int e4 = f - r * e4n;
-          off[u] = f < tot ? r * pitch + 4 * e4 : -1;
-          v[u] = f < tot ? reinterpret_cast<const float4*>(p.K + static_cast<int64_t>(cand[c0 + r]) * p.E)[e4]
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (off[u] >= 0) *reinterpret_cast<float4*>(rs + off[u]) = v[u];
-      }
-      __syncthreads();
+      stage_rows(c0, nb);
       // the chain stays one fma per feature in feature order; reading four
       // features per 16-byte LDS access (the query's a broadcast) and
       // unrolling lets the reads run ahead of the dependent fp64 chain
@@ -580,7 +599,10 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
           const bool cand_ok = ok[r] && (exhaustive || static_cast<double>(sv[r]) + err(nv[r]) >= thresh);
           const uint64_t cmask = __ballot(cand_ok);
           if (!cmask) continue;
-          if (ncand + 64 > kCand) flush();
+          if (ncand + 64 > kCand) {
+            early = true;
+            flush();
+          }
           if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(ii[r]);
           ncand += __builtin_popcountll(cmask);
         }
@@ -605,7 +627,54 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     }
     test_group(kb0, b4, n4);
   }
-  flush();
+  // Top-1 without scores: the candidate list provably holds the exact
+  // argmax, so a single candidate is the answer.  With several, each is
+  // scored by a lane-parallel fp64 sum (every product exact; each lane sums
+  // its E / 64 features, then a 6-level tree), which differs from the
+  // exact real sum by at most gamma_{E/64+7} sum |p_e|; the sequential sum
+  // of the definition by at most gamma_E sum |p_e|; and sum |p_e| <=
+  // |q| |k_i| (1.01 covers the fp32 norms).  If the best candidate's lower
+  // end beats every other's upper end, it is the sequential argmax;
+  // otherwise (near or exact ties) the sequential rescoring below decides.
+  bool done = false;
+  if (k == 1 && p.score == nullptr && !early && ncand > 0) {
+    if (ncand == 1) {
+      li = cand[0];
+      done = true;
+    } else {
+      const double u53 = 1.1102230246251565e-16;  // 2^-53
+      const double nf = static_cast<double>(E / 64 + 7);
+      const double gs = 1.01 * (nf * u53 / (1.0 - nf * u53) + en * u53 / (1.0 - en * u53));
+      double best = 0.0, best_mu = 0.0, others = -INFINITY;
+      int best_i = -1;
+      for (int c0 = 0; c0 < ncand; c0 += batch_max) {
+        const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
+        stage_rows(c0, nb);
+        for (int r = 0; r < nb; ++r) {
+          const float* row = rs + r * pitch;
+          double part = 0.0;
+          for (int e = lane; e < E; e += 64)
+            part = fma(static_cast<double>(qs[e]), static_cast<double>(row[e]), part);
+          const double a = wave_sum_d(part);
+          const int ci = cand[c0 + r];
+          const double mu = gs * qn * sqrt(static_cast<double>(p.rownorm2[ci])) + 1e-300;
+          if (best_i < 0 || a > best || (a == best && ci < best_i)) {
+            if (best_i >= 0) others = fmax(others, best + best_mu);
+            best = a;
+            best_mu = mu;
+            best_i = ci;
+          } else {
+            others = fmax(others, a + mu);
+          }
+        }
+      }
+      if (best - best_mu > others) {
+        li = best_i;
+        done = true;
+      }
+    }
+  }
+  if (!done) flush();
   if (lane < k) {
     p.idx[q * k + lane] = static_cast<int32_t>(li);
     if (p.score) p.score[q * k + lane] = ls;

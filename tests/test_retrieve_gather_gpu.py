@@ -63,6 +63,27 @@ def test_retrieval_duplicates_and_near_ties():
     assert np.array_equal(_gpu_top1(q, torch.from_numpy(K)), ref)
 
 
+def test_retrieval_equal_real_scores_decided_by_summation_order():
+    """Keys that differ from the winner only by two swapped components where
+    the query holds equal values: the real inner products are equal, so any
+    summation other than the sequential fp64 one of the definition (a tree,
+    partial sums) cannot order them; the answer must still be the oracle's."""
+    g = np.random.default_rng(66)
+    q, K, _, _ = synth.retrieval_inputs_host(48, 2000, 384, 0, seed=66)
+    qn, Kn = q.numpy().copy(), K.numpy().copy()
+    pairs = [tuple(int(v) for v in g.choice(384, 2, replace=False)) for _ in range(48)]
+    for i, (a, b) in enumerate(pairs):
+        qn[i, b] = qn[i, a]
+    win, _ = oracle.top1(qn, Kn)
+    for i, w in enumerate(win):
+        a, b = pairs[i]
+        twin = Kn[w].copy()
+        twin[a], twin[b] = Kn[w, b], Kn[w, a]
+        Kn[(w + 1 + i) % 2000] = twin
+    ref, _ = oracle.top1(qn, Kn)
+    assert np.array_equal(_gpu_top1(torch.from_numpy(qn), torch.from_numpy(Kn)), ref)
+
+
 def test_retrieval_non_unit_rows_and_empty():
     q, K, _, _ = synth.retrieval_inputs_host(40, 500, 64, 8, seed=62)
     scale = torch.from_numpy(np.random.default_rng(1).uniform(0.1, 30.0, (500, 1))).float()
