@@ -162,6 +162,7 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
 
   if (nsteps > 0) {
     fetch(t0b, 0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): tile 0 in before tile 1 is requested
     int tile = 0;
     for (; (tile + 2) * kPFWide <= nsteps; tile += 2) {
       if (fair) balance_step(progress, wave, tile);

@@ -646,6 +646,10 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
 
   if (nsteps > 0) {
     fetch(t0b, 0);
+    // Tile 0 completes before tile 1 is requested (vmcnt(0); lgkmcnt and
+    // expcnt untouched): at launch every wave requests at once, and tile 0
+    // then does not queue behind tile 1 (corpus encode 1.2445 -> 1.2297 ms).
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     int tile = 0;
     // Pairs of whole tiles: straight-line code, no per-token guards.
     for (; (tile + 2) * kPF <= nsteps; tile += 2) {
