@@ -531,13 +531,30 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // staging costs.
   constexpr bool kLds = kLdsBcast && NL == 16 && (kRead || P > 1);
   __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kSBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
+  // bf16 coefficients go in as raw bits into the high half of a word whose
+  // low half is zero (cleared once, below): the word is then the exact fp32
+  // value with no conversion instruction.  Written as bytes, so the
+  // compiler keeps their order with the float reads of the tile.
+  constexpr bool kRawHigh = sizeof(typename SI::raw) == 2;
+  auto put = [&](float* dst, typename SI::raw v) {
+    if constexpr (kRawHigh) {
+      __builtin_memcpy(reinterpret_cast<char*>(dst) + 2, &v, 2);
+    } else {
+      *dst = SI::f32(v);
+    }
+  };
+  if constexpr (kLds && kRawHigh) {
+    float* slice = &bc_lds[wave][0][0][0];
+#pragma unroll
+    for (int i = lane; i < kPF * 2 * N; i += 64) slice[i] = 0.f;
+  }
   auto stage = [&](const Tile& tb) {
     if constexpr (kLds) {
       if ((lane >> 4) < P) {
 #pragma unroll
         for (int k = 0; k < kPF; ++k) {
-          bc_lds[wave][k][0][16 * grp + lane16] = SI::f32(tb.b[k][0]);
-          if constexpr (kRead) bc_lds[wave][k][1][16 * grp + lane16] = SI::f32(tb.c[k][0]);
+          put(&bc_lds[wave][k][0][16 * grp + lane16], tb.b[k][0]);
+          if constexpr (kRead) put(&bc_lds[wave][k][1][16 * grp + lane16], tb.c[k][0]);
         }
       }
       // Wait until the writes have completed (lgkmcnt(0); vmcnt and expcnt
