@@ -62,6 +62,39 @@ def test_route_ties_go_to_lower_index():
     assert m[0] == 1 and j[0] == 0
 
 
+def test_route_equal_real_scores_decided_by_summation_order():
+    """Prototypes that differ from the winning one only by two swapped
+    components where the embedding holds equal values: equal real inner
+    products, so only the sequential fp64 sums of the definition can order
+    them (both stages, staged-row path)."""
+    g = np.random.default_rng(67)
+    C, E, nd, ns = 40, 384, 5, 4
+    emb = synth.unit_rows_host(C, E, g)
+    pairs = [tuple(int(v) for v in g.choice(E, 2, replace=False)) for _ in range(C)]
+    for i, (a, b) in enumerate(pairs):
+        emb[i, b] = emb[i, a]
+    outs = []
+    for i in range(C):
+        # one embedding per call: its own prototype set with twinned winners
+        dom = synth.unit_rows_host(nd, E, g)
+        sub = synth.unit_rows_host(nd * ns, E, g).reshape(nd, ns, E)
+        rm, _ = oracle.route2(emb[i:i + 1], dom, sub)
+        w = int(rm[0])
+        a, b = pairs[i]
+        twin = dom[w].copy()
+        twin[a], twin[b] = dom[w, b], dom[w, a]
+        dom[(w + 1) % nd] = twin
+        rm, rj = oracle.route2(emb[i:i + 1], dom, sub)
+        sw = int(rj[0])
+        st = sub[int(rm[0]), sw].copy()
+        st[a], st[b] = sub[int(rm[0]), sw, b], sub[int(rm[0]), sw, a]
+        sub[int(rm[0]), (sw + 1) % ns] = st
+        rm, rj = oracle.route2(emb[i:i + 1], dom, sub)
+        m, j, _ = _route(*(torch.from_numpy(np.ascontiguousarray(x)) for x in (emb[i:i + 1], dom, sub)))
+        outs.append((m[0] == rm[0]) and (j[0] == rj[0]))
+    assert all(outs)
+
+
 def _cons_bound(states0, contrib, target, alpha, mag_unit):
     """Per-row bound: each fp32 update adds at most 3 units of 2^-24 of the
     magnitudes involved (two roundings of the factors, one of the fused
