@@ -20,6 +20,8 @@
  *   precog_scan_complex     Eq. 1 with a diagonal complex A (Sec. 3)
  * the top-k extension of retrieval and injection:
  *   precog_retrieve_topk    exact top-k with scores (Sec. 4.4, Fig. 1)
+ *   precog_retrieve_prepare / precog_retrieve_topk_prepared
+ *                           the same retrieval over an index prepared once
  *   precog_inject_compose   softmax-weighted composition of the top-k states
  *                           (Sec. 5.4 Eq. smc-fusion)
  * and the memory-consolidation steps of SMC:
@@ -263,6 +265,42 @@ precog_status precog_retrieve_topk(const float *query_emb,
                                    int64_t E, int64_t k, int32_t *idx,
                                    double *score, void *workspace,
                                    size_t workspace_bytes, void *stream);
+
+/* Prepared index (the offline side of Sec. 4.2: keys are embedded once).
+ * Bytes of the prepared form of an [M, E] key index: the keys' fp16(2^8 k)
+ * screen operands in the screen's own tile order, their squared norms and
+ * the largest squared norm of every 32-key block.  0 for M < 1 or an E the
+ * retrieval calls reject. */
+size_t precog_retrieve_index_bytes(int64_t M, int64_t E);
+
+/* Writes the prepared form of index_emb ([M, E] fp32, the same rows the
+ * retrieval calls read) into `prepared` (device memory, caller-owned,
+ * precog_retrieve_index_bytes(M, E) bytes, 16-byte aligned).  Asynchronous
+ * on `stream`; the prepared form stays valid while index_emb is unchanged.
+ *   1 <= M < 2^31, 4 <= E <= 4096, E % 4 == 0, else PRECOG_ERR_SHAPE /
+ *   PRECOG_ERR_ALIGN; too small a buffer gives PRECOG_ERR_WORKSPACE. */
+precog_status precog_retrieve_prepare(const float *index_emb, int64_t M,
+                                      int64_t E, void *prepared,
+                                      size_t prepared_bytes, void *stream);
+
+/* precog_retrieve_topk (and, with k = 1 and score NULL, precog_retrieve_top1)
+ * with the screen reading the prepared operands and norms instead of
+ * converting index_emb on every call.  Results are identical to the
+ * unprepared calls: the same operands, the same margin, the same fp64
+ * decision over index_emb's fp32 rows (which must be the rows `prepared`
+ * was made from).  Arguments as precog_retrieve_topk, plus
+ *   prepared   from precog_retrieve_prepare(index_emb, M, E, ...), 16-byte
+ *              aligned, prepared_bytes >= precog_retrieve_index_bytes(M, E)
+ *              (else PRECOG_ERR_WORKSPACE; NULL gives PRECOG_ERR_NULL). */
+precog_status precog_retrieve_topk_prepared(const float *query_emb,
+                                            const float *index_emb,
+                                            const void *prepared,
+                                            size_t prepared_bytes, int64_t Q,
+                                            int64_t M, int64_t E, int64_t k,
+                                            int32_t *idx, double *score,
+                                            void *workspace,
+                                            size_t workspace_bytes,
+                                            void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* State injection                                                          */

@@ -314,9 +314,59 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E) {
 }
 
 namespace {
-precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q, int64_t M,
-                       int64_t E, int64_t k, int32_t* idx, double* score, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+// Prepared index: operands [nkb, nks, 2, 32] x 16 B, squared key norms [M],
+// block norm maxima [nkb], each 256-byte aligned.
+struct IndexLayout {
+  size_t ops, rownorm, blocknorm, total;
+};
+IndexLayout index_layout(int64_t M, int64_t E) {
+  IndexLayout l;
+  const size_t nkb = static_cast<size_t>((M + 31) / 32);
+  const size_t nks = static_cast<size_t>((E + 15) / 16);
+  l.ops = align_up(nkb * nks * 64 * 16);
+  l.rownorm = align_up(static_cast<size_t>(M) * 4);
+  l.blocknorm = align_up(nkb * 4);
+  l.total = l.ops + l.rownorm + l.blocknorm;
+  return l;
+}
+}  // namespace
+
+size_t precog_retrieve_index_bytes(int64_t M, int64_t E) {
+  if (M < 1 || E < 4 || E > 4096 || E % 4 != 0 || M > 0x7fffffffLL) return 0;
+  return index_layout(M, E).total;
+}
+
+precog_status precog_retrieve_prepare(const float* index_emb, int64_t M, int64_t E, void* prepared,
+                                      size_t prepared_bytes, void* stream) {
+  if (M < 1 || E < 4 || E > 4096 || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (E % 4 != 0) return PRECOG_ERR_ALIGN;
+  if (!index_emb || !prepared) return PRECOG_ERR_NULL;
+  if (!aligned16(index_emb) || !aligned16(prepared)) return PRECOG_ERR_ALIGN;
+  if (prepared_bytes < precog_retrieve_index_bytes(M, E)) return PRECOG_ERR_WORKSPACE;
+  const int64_t nkb = ceil_div(M, 32);
+  if (nkb * ((E + 15) / 16) * 64 / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+  const IndexLayout l = index_layout(M, E);
+  char* at = static_cast<char*>(prepared);
+  precog::RetrieveParams p{};
+  p.K = index_emb;
+  p.kop = at;
+  p.rownorm2 = reinterpret_cast<float*>(at + l.ops);
+  p.blocknorm2 = reinterpret_cast<float*>(at + l.ops + l.rownorm);
+  p.M = M;
+  p.E = E;
+  p.nkb = static_cast<int>(nkb);
+  p.nks = static_cast<int>((E + 15) / 16);
+  (void)hipGetLastError();
+  const hipError_t e = precog::launch_retrieve_prepare(p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+}
+
+namespace {
+precog_status retrieve(const float* query_emb, const float* index_emb, const void* prepared,
+                       int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx, double* score,
+                       void* workspace, size_t workspace_bytes, void* stream) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
@@ -325,7 +375,7 @@ precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q
   if (Q == 0) return PRECOG_OK;
   if (!query_emb || !idx) return PRECOG_ERR_NULL;
   if (M > 0 && !index_emb) return PRECOG_ERR_NULL;
-  const void* ptrs[] = {query_emb, index_emb, idx, workspace, score};
+  const void* ptrs[] = {query_emb, index_emb, idx, workspace, score, prepared};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
   const size_t need = precog_retrieve_workspace_bytes(Q, M, E);
@@ -348,6 +398,14 @@ precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q
     p.rownorm2 = reinterpret_cast<float*>(at);
     at += w.rownorm;
     p.blocknorm2 = reinterpret_cast<float*>(at);
+    if (prepared) {
+      // operands and norms from the prepared index
+      const IndexLayout l = index_layout(M, E);
+      const char* pb = static_cast<const char*>(prepared);
+      p.kop = pb;
+      p.rownorm2 = reinterpret_cast<float*>(const_cast<char*>(pb + l.ops));
+      p.blocknorm2 = reinterpret_cast<float*>(const_cast<char*>(pb + l.ops + l.rownorm));
+    }
   }
   p.idx = idx;
   p.score = score;
@@ -368,16 +426,28 @@ precog_status retrieve(const float* query_emb, const float* index_emb, int64_t Q
 precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
                                    int64_t M, int64_t E, int32_t* idx, void* workspace,
                                    size_t workspace_bytes, void* stream) {
-  return retrieve(query_emb, index_emb, Q, M, E, 1, idx, nullptr, workspace, workspace_bytes,
-                  stream);
+  return retrieve(query_emb, index_emb, nullptr, Q, M, E, 1, idx, nullptr, workspace,
+                  workspace_bytes, stream);
 }
 
 precog_status precog_retrieve_topk(const float* query_emb, const float* index_emb, int64_t Q,
                                    int64_t M, int64_t E, int64_t k, int32_t* idx, double* score,
                                    void* workspace, size_t workspace_bytes, void* stream) {
   if (k < 1 || k > precog::kMaxTopK || k > M) return PRECOG_ERR_SHAPE;
-  return retrieve(query_emb, index_emb, Q, M, E, k, idx, score, workspace, workspace_bytes,
-                  stream);
+  return retrieve(query_emb, index_emb, nullptr, Q, M, E, k, idx, score, workspace,
+                  workspace_bytes, stream);
+}
+
+precog_status precog_retrieve_topk_prepared(const float* query_emb, const float* index_emb,
+                                            const void* prepared, size_t prepared_bytes, int64_t Q,
+                                            int64_t M, int64_t E, int64_t k, int32_t* idx,
+                                            double* score, void* workspace, size_t workspace_bytes,
+                                            void* stream) {
+  if (k < 1 || k > precog::kMaxTopK || k > M) return PRECOG_ERR_SHAPE;
+  if (!prepared) return PRECOG_ERR_NULL;
+  if (prepared_bytes < precog_retrieve_index_bytes(M, E)) return PRECOG_ERR_WORKSPACE;
+  return retrieve(query_emb, index_emb, prepared, Q, M, E, k, idx, score, workspace,
+                  workspace_bytes, stream);
 }
 
 precog_status precog_inject_gather(const void* state_store, precog_dtype store_dtype, int64_t M,

@@ -71,6 +71,7 @@ struct RetrieveParams {
   const float* q;      // [Q, E]
   const float* K;      // [M, E]
   void* qop;           // fp16(2^8 q) in operand order (workspace)
+  const void* kop;     // prepared index operands, or null (keys read as fp32)
   float* scores;       // [Q, ld_scores] screen scores (workspace)
   float* blockmax;     // [Q, nkb] max screen score per 32-key block (workspace)
   float* rownorm2;     // [M] squared key norms (workspace)
@@ -86,6 +87,8 @@ struct RetrieveParams {
 };
 constexpr int kMaxTopK = 64;
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
+// Prepared index: p.kop, p.rownorm2 and p.blocknorm2 are written from p.K.
+hipError_t launch_retrieve_prepare(const RetrieveParams& p, hipStream_t s);
 
 struct GatherParams {
   const void* store;  // [M, S]

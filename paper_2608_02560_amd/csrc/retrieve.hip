@@ -161,6 +161,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const RetrieveParams p) {
 // product is unchanged whatever order the instruction consumes features in.
 // Output register r holds query row 8 (r / 4) + 4 h + (r mod 4), key column
 // l mod 32; screen scores are stored as 128-byte runs of 32 keys.
+template <bool PREP>
 __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
   const int nqwg = static_cast<int>((p.Q + kQWG - 1) / kQWG);
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
@@ -210,13 +211,27 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
     // t mod 4 + 4 (t / 128) + 8 j, so four lanes read 64 contiguous bytes
     // of a row and the wave covers 16 rows per load), then the wave's query
     // operands (entries past the group's nks read as zero)
-    float4 kv[kFC / 32];
+    // prepared index: the chunk's tile is a contiguous run of nks x 64
+    // operand entries, already in the LDS order (swizzle included)
+    constexpr int kPK = kKS * 64 / 256;  // prepared entries per thread per chunk
+    halfx8 pk[PREP ? kPK : 1];
+    float4 kv[PREP ? 1 : kFC / 32];
+    if constexpr (PREP) {
+      const halfx8* src = static_cast<const halfx8*>(p.kop) +
+                          (static_cast<int64_t>(kb) * p.nks + fc / 16) * 64;
 #pragma unroll
-    for (int j = 0; j < kFC / 32; ++j) {
-      const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
-      const int64_t e = fc + 4 * c4;
-      const uint32_t off = e < E ? krow_off + static_cast<uint32_t>(e * 4) : kDropOffset;
-      kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
+      for (int j = 0; j < kPK; ++j) {
+        const int i = tid + 256 * j;
+        if (i < nks * 64) pk[j] = src[i];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kFC / 32; ++j) {
+        const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
+        const int64_t e = fc + 4 * c4;
+        const uint32_t off = e < E ? krow_off + static_cast<uint32_t>(e * 4) : kDropOffset;
+        kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
+      }
     }
     halfx8 aq[kKS];
 #pragma unroll
@@ -224,16 +239,25 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
       const uint32_t so = (ks0 + ks) * 1024u;
       aq[ks] = __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(ores, lane_off, so, 0));
     }
+    if constexpr (PREP) {
+      halfx8* dst = &kop[buf][0][0][0];
 #pragma unroll
-    for (int j = 0; j < kFC / 32; ++j) {
-      const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
-      const float4 v = kv[j];
-      n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
-      const int ks = c4 >> 2;
-      const int h = (c4 >> 1) & 1;
-      const int sub = c4 & 1;
-      const int srow = srow_base ^ ((2 * ks + h) & 31);
-      reinterpret_cast<halfx4*>(&kop[buf][ks][h][srow])[sub] = to_op(v);
+      for (int j = 0; j < kPK; ++j) {
+        const int i = tid + 256 * j;
+        if (i < nks * 64) dst[i] = pk[j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kFC / 32; ++j) {
+        const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
+        const float4 v = kv[j];
+        n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
+        const int ks = c4 >> 2;
+        const int h = (c4 >> 1) & 1;
+        const int sub = c4 & 1;
+        const int srow = srow_base ^ ((2 * ks + h) & 31);
+        reinterpret_cast<halfx4*>(&kop[buf][ks][h][srow])[sub] = to_op(v);
+      }
     }
     __syncthreads();
     if (active) {
@@ -275,9 +299,10 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
       }
     }
   }
-  // squared key norms (workgroups with qg == 0): the eight threads staging
-  // a row hold disjoint parts of it; combined in a fixed order
-  if (qg == 0) {
+  // squared key norms (workgroups with qg == 0; a prepared index holds
+  // them): the eight threads staging a row hold disjoint parts of it;
+  // combined in a fixed order
+  if (!PREP && qg == 0) {
     n2 += xor_shfl(n2, 1);
     n2 += xor_shfl(n2, 2);
     if ((tid & 3) == 0) nsum[tid >> 7][srow_base] = n2;
@@ -298,6 +323,56 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
 }
 
 // the rank order: larger score first, then lower index
+// Prepared index, operands: entry ((kb * nks + ks) * 2 + h) * 32 + r' holds
+// features [16 ks + 8 h, 16 ks + 8 h + 8) of key 32 kb + r as fp16(2^8 k)
+// (zero past M or E), at r' = r xor ((2 (ks mod kKS) + h) mod 32): the order
+// and swizzle of the screen's LDS tile, so a chunk's tile is one contiguous
+// copy.
+__global__ __launch_bounds__(256) void prep_index_kernel(const RetrieveParams p) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t total = static_cast<int64_t>(p.nkb) * p.nks * 64;
+  if (t >= total) return;
+  const int r = static_cast<int>(t & 31);
+  const int h = static_cast<int>((t >> 5) & 1);
+  const int64_t bk = t >> 6;
+  const int ks = static_cast<int>(bk % p.nks);
+  const int64_t kb = bk / p.nks;
+  const int64_t key = kb * kKB + r;
+  halfx4 o[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int64_t e = 16 * ks + 8 * h + 4 * c;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (key < p.M && e < p.E) v = *reinterpret_cast<const float4*>(p.K + key * p.E + e);
+    o[c] = to_op(v);
+  }
+  const int rs = r ^ ((2 * (ks % kKS) + h) & 31);
+  const halfx8 o8 = {o[0][0], o[0][1], o[0][2], o[0][3], o[1][0], o[1][1], o[1][2], o[1][3]};
+  static_cast<halfx8*>(const_cast<void*>(p.kop))[(bk * 2 + h) * 32 + rs] = o8;
+}
+
+// Prepared index, norms: one wave per 32-key block; lane l < 32 sums the
+// squares of key 32 kb + l, the block keeps the largest.
+__global__ __launch_bounds__(64) void prep_norms_kernel(const RetrieveParams p) {
+  const int64_t kb = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t key = kb * kKB + (lane & 31);
+  const bool ok = lane < kKB && key < p.M;
+  float n2 = 0.f;
+  if (ok) {
+    const float4* row = reinterpret_cast<const float4*>(p.K + key * p.E);
+    for (int64_t e4 = 0; e4 < p.E / 4; ++e4) {
+      const float4 v = row[e4];
+      n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
+    }
+    p.rownorm2[key] = n2;
+  }
+  float mx = ok ? n2 : 0.f;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) mx = fmaxf(mx, xor_shfl(mx, m));
+  if (lane == 0) p.blocknorm2[kb] = mx;
+}
+
 __device__ __forceinline__ bool ranks_before(double s, int i, double bs, int bi) {
   return s > bs || (s == bs && i < bi);
 }
@@ -688,9 +763,20 @@ hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s) {
     const int64_t entries = static_cast<int64_t>(p.nqg) * p.nks * 64;
     hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, s, p);
     const int64_t nqwg = (p.Q + kQWG - 1) / kQWG;
-    hipLaunchKernelGGL(screen_kernel, dim3(static_cast<unsigned>(p.nkb * nqwg)), dim3(256), 0, s, p);
+    const dim3 grid(static_cast<unsigned>(p.nkb * nqwg));
+    if (p.kop != nullptr)
+      hipLaunchKernelGGL(screen_kernel<true>, grid, dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL(screen_kernel<false>, grid, dim3(256), 0, s, p);
   }
   hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_retrieve_prepare(const RetrieveParams& p, hipStream_t s) {
+  const int64_t entries = static_cast<int64_t>(p.nkb) * p.nks * 64;
+  hipLaunchKernelGGL(prep_index_kernel, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(prep_norms_kernel, dim3(static_cast<unsigned>(p.nkb)), dim3(64), 0, s, p);
   return hipGetLastError();
 }
 

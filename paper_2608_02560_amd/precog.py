@@ -28,7 +28,8 @@ EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_enc
            "precog_scan_trajectory",
            "precog_scan_complex",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
-           "precog_retrieve_topk", "precog_inject_gather", "precog_inject_compose",
+           "precog_retrieve_topk", "precog_retrieve_index_bytes", "precog_retrieve_prepare",
+           "precog_retrieve_topk_prepared", "precog_inject_gather", "precog_inject_compose",
            "precog_smc_route", "precog_smc_consolidate", "precog_status_string")
 
 
@@ -78,6 +79,13 @@ def lib():
         L.precog_retrieve_top1.restype = ctypes.c_int
         L.precog_retrieve_topk.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
         L.precog_retrieve_topk.restype = ctypes.c_int
+        L.precog_retrieve_index_bytes.argtypes = [i64, i64]
+        L.precog_retrieve_index_bytes.restype = sz
+        L.precog_retrieve_prepare.argtypes = [vp, i64, i64, vp, sz, vp]
+        L.precog_retrieve_prepare.restype = ctypes.c_int
+        L.precog_retrieve_topk_prepared.argtypes = [vp, vp, vp, sz, i64, i64, i64, i64, vp, vp, vp,
+                                                    sz, vp]
+        L.precog_retrieve_topk_prepared.restype = ctypes.c_int
         L.precog_inject_gather.argtypes = [vp, ctypes.c_int, i64, i64, vp, i64, vp,
                                            ctypes.c_int, vp]
         L.precog_inject_gather.restype = ctypes.c_int
@@ -193,6 +201,33 @@ def retrieve_topk(query, index, k, idx, score, workspace, workspace_bytes=None, 
                                     _ptr(score), _ptr(workspace), int(workspace_bytes),
                                     _stream(stream))
     _check("precog_retrieve_topk", st)
+
+
+def retrieve_index_bytes(M, E) -> int:
+    return int(lib().precog_retrieve_index_bytes(M, E))
+
+
+def retrieve_prepare(index, prepared, stream=None):
+    """precog_retrieve_prepare: the prepared form of index [M, E] into `prepared`."""
+    M, E = index.shape
+    nbytes = prepared.numel() * prepared.element_size()
+    st = lib().precog_retrieve_prepare(_ptr(index), M, E, _ptr(prepared), int(nbytes),
+                                       _stream(stream))
+    _check("precog_retrieve_prepare", st)
+
+
+def retrieve_topk_prepared(query, index, prepared, k, idx, score, workspace, workspace_bytes=None,
+                           stream=None):
+    Q, E = query.shape
+    M = index.shape[0]
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    pbytes = prepared.numel() * prepared.element_size()
+    st = lib().precog_retrieve_topk_prepared(_ptr(query), _ptr(index), _ptr(prepared), int(pbytes),
+                                             Q, M, E, int(k), _ptr(idx), _ptr(score),
+                                             _ptr(workspace), int(workspace_bytes),
+                                             _stream(stream))
+    _check("precog_retrieve_topk_prepared", st)
 
 
 def inject_compose(store, idx, score, tau, h0, stream=None):
@@ -321,6 +356,27 @@ def topk(query, index, k, stream=None):
     nbytes = retrieve_workspace_bytes(Q, M, E)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=query.device)
     retrieve_topk(query, index, k, idx, score, ws, nbytes, stream)
+    return idx, score
+
+
+def prepare_index(index, stream=None):
+    """The prepared form of index [M, E] (a uint8 device tensor)."""
+    M, E = index.shape
+    prepared = torch.empty(max(retrieve_index_bytes(M, E), 16), dtype=torch.uint8,
+                           device=index.device)
+    retrieve_prepare(index, prepared, stream)
+    return prepared
+
+
+def topk_prepared(query, index, prepared, k, want_score=True, stream=None):
+    """Exact top-k over a prepared index: (idx int32 [Q, k], score fp64 [Q, k] or None)."""
+    Q, E = query.shape
+    M = index.shape[0]
+    idx = torch.empty((Q, k), dtype=torch.int32, device=query.device)
+    score = torch.empty((Q, k), dtype=torch.float64, device=query.device) if want_score else None
+    nbytes = retrieve_workspace_bytes(Q, M, E)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=query.device)
+    retrieve_topk_prepared(query, index, prepared, k, idx, score, ws, nbytes, stream)
     return idx, score
 
 

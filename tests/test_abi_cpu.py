@@ -191,6 +191,36 @@ def test_topk_validation_errors():
     assert call(Q=0) == OK
 
 
+def test_prepared_index_validation_errors():
+    L = P.lib()
+    nb = P.retrieve_index_bytes(10, 16)
+    # 16-byte operand entries for ceil(10/32) blocks x ceil(16/16) steps x 64,
+    # then the norms, each part 256-byte aligned
+    assert nb == 1024 + 256 + 256
+    assert P.retrieve_index_bytes(0, 16) == 0
+    assert P.retrieve_index_bytes(10, 18) == 0
+    prep = lambda K=FAKE, M=10, E=16, out=FAKE, b=nb: L.precog_retrieve_prepare(K, M, E, out, b, None)
+    assert prep(M=0) == ESHAPE
+    assert prep(E=4100) == ESHAPE
+    assert prep(E=18) == EALIGN
+    assert prep(K=None) == ENULL
+    assert prep(out=None) == ENULL
+    assert prep(out=FAKE + 8) == EALIGN
+    assert prep(b=nb - 1) == EWS
+    ws = P.retrieve_workspace_bytes(4, 10, 16)
+    call = lambda q=FAKE, K=FAKE, pr=FAKE, pb=nb, Q=4, M=10, E=16, k=3, idx=FAKE, sc=FAKE, \
+        w=FAKE, wb=ws: L.precog_retrieve_topk_prepared(q, K, pr, pb, Q, M, E, k, idx, sc, w, wb,
+                                                       None)
+    assert call(k=0) == ESHAPE
+    assert call(k=11) == ESHAPE
+    assert call(pr=None) == ENULL
+    assert call(pb=nb - 1) == EWS
+    assert call(pr=FAKE + 8) == EALIGN
+    assert call(E=18) == EALIGN
+    assert call(w=None) == EWS
+    assert call(Q=0) == OK
+
+
 def test_compose_validation_errors():
     L = P.lib()
     call = lambda s=FAKE, sd=P.F16, M=10, S=64, idx=FAKE, sc=FAKE, Q=3, k=3, tau=1.0, h=FAKE, \

@@ -135,6 +135,36 @@ def test_retrieval_components_below_fp16_normal_range():
     assert np.array_equal(_gpu_top1(torch.from_numpy(qn), torch.from_numpy(Kn)), ref)
 
 
+@pytest.mark.parametrize("Q,M,E", [(256, 10000, 384), (65, 1000, 20), (70, 97, 388),
+                                   (5, 70001, 8), (40, 300, 4096), (3, 33, 16)])
+def test_prepared_index_equals_unprepared(Q, M, E):
+    """The prepared index (operands and norms made once) gives the indices
+    and fp64 scores of the unprepared calls bit for bit, and the oracle's."""
+    q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 4), seed=Q + 3 * M + E)
+    qd, Kd = q.to(DEV), K.to(DEV)
+    prepared = P.prepare_index(Kd)
+    for k in (1, 3):
+        i0, s0 = P.topk(qd, Kd, k)
+        i1, s1 = P.topk_prepared(qd, Kd, prepared, k)
+        torch.cuda.synchronize()
+        assert torch.equal(i0, i1) and torch.equal(s0, s1), k
+    i2, _ = P.topk_prepared(qd, Kd, prepared, 1, want_score=False)
+    torch.cuda.synchronize()
+    ref, _ = oracle.top1(q, K, nthreads=8)
+    assert np.array_equal(i2[:, 0].cpu().numpy(), ref)
+
+
+def test_prepared_index_norms_past_the_screen_range():
+    q, K, _, _ = synth.retrieval_inputs_host(24, 700, 128, 4, seed=65)
+    K2 = K.clone()
+    K2[::97] *= 1000.0
+    prepared = P.prepare_index(K2.to(DEV))
+    i1, _ = P.topk_prepared(q.to(DEV), K2.to(DEV), prepared, 1, want_score=False)
+    torch.cuda.synchronize()
+    ref, _ = oracle.top1(q, K2)
+    assert np.array_equal(i1[:, 0].cpu().numpy(), ref)
+
+
 @pytest.mark.parametrize("sd,od", [(torch.float16, torch.float16), (torch.float16, torch.float32),
                                    (torch.float32, torch.float32), (torch.float32, torch.float16)])
 def test_gather_dtypes(sd, od):
