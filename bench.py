@@ -27,6 +27,10 @@ if ROOT not in sys.path:
 
 METRIC = "SSM prefill scan tokens/s & achieved HBM GB/s (fraction of peak), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+# v_exp_f32 issues at a quarter of the fp32 slot rate: the 157.3 TFLOP/s
+# vector peak is 7.86e13 slots/s x 2 flops, so 1.97e13 exp/s (measured on
+# the box: ~8 cycles per wave64 v_exp_f32 per SIMD at 8 waves, the same)
+EXP_PEAK_PER_S = 157.3e12 / 2 / 4
 # MI355X fp32 vector peak: 157.3 TFLOP/s = 7.86e13 FMA issue slots/s (256 CUs x
 # 2.4 GHz x 128 lanes).  The scan's algorithmic work per (token, channel,
 # state) is 8 issue slots: v_mul (dt A'), v_exp_f32 (quarter rate: 4 slots),
@@ -193,6 +197,10 @@ def bench_corpus(args):
                      "work": "16 FMA-equivalent flops (8 fp32 issue slots) per (t, d, n)"},
         "hbm": {"achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBPS, "bytes_per_launch": nbytes},
+        # decays exp(-dt A): one v_exp_f32 per (t, d, n); the peak is the
+        # quarter-rate transcendental issue of 1024 SIMDs at 2.4 GHz
+        "exp": {"achieved": B * L * D * N / (ev_ms * 1e-3), "peak": EXP_PEAK_PER_S,
+                "unit": "exp/s", "frac": B * L * D * N / (ev_ms * 1e-3) / EXP_PEAK_PER_S},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline_corpus(inp, wl, args.cpu_rows)
