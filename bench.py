@@ -459,7 +459,10 @@ def bench_extra(args):
     res["large_corpus_layer"] = {"workload": wl.name, "ms": c_ms,
                                  "tokens_per_s": B * L / (c_ms * 1e-3),
                                  "gbps": nb / (c_ms * 1e-3) / 1e9,
-                                 "exp_per_s": B * L * D * N / (c_ms * 1e-3)}
+                                 "exp_per_s": B * L * D * N / (c_ms * 1e-3),
+                                 "exp_frac": B * L * D * N / (c_ms * 1e-3) / EXP_PEAK_PER_S,
+                                 # all 24 layers of a chunk batch, one layer per launch
+                                 "chunk_tokens_per_s_24_layers": B * L / (24 * c_ms * 1e-3)}
     return res
 
 
