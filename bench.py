@@ -132,7 +132,20 @@ def cpu_baseline_corpus(inp, wl, rows_b):
     tokens = rows_b * wl.seqlen
     return {"value": tokens / dt, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
             "sample": "%d of %d chunks x %d tokens x %d channels, N=%d, fp64, %.1f s wall"
-                      % (rows_b, wl.batch, wl.seqlen, wl.dim, wl.dstate, dt)}
+                      % (rows_b, wl.batch, wl.seqlen, wl.dim, wl.dstate, dt),
+            "cpu": cpu_model()}
+
+
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def bench_corpus(args):
