@@ -387,6 +387,7 @@ __device__ __forceinline__ bool before(float v, int i, float bv, int bi) {
 }
 
 constexpr int kCand = 256;            // candidate list capacity (indices)
+constexpr int kBList = 512;           // surviving-block list capacity (>= 2 groups of 256)
 // squared norm below which 2^8 |v| stays under the fp16 overflow threshold
 // for every component v (|v| < 245)
 constexpr float kMaxNorm2 = 60000.f;
@@ -416,6 +417,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   __shared__ __attribute__((aligned(16))) float qs[kMaxE];
   __shared__ __attribute__((aligned(16))) float rs[kRowWords];
   __shared__ int cand[kCand];
+  __shared__ int blist[kBList];
   __shared__ double slot_s[64];
   __shared__ int slot_i[64];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
@@ -635,53 +637,57 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     ncand = 0;
   };
 
+  // surviving blocks go, in ascending order, to an LDS list whose keys are
+  // tested eight blocks per round (two per 64-lane pass, so their score and
+  // norm loads are in flight together), whatever 64-block slices they came
+  // from: a query whose few surviving blocks lie in different slices pays
+  // one round, not one per slice
+  int nbl = 0;
+  auto test_list = [&]() __attribute__((always_inline)) {
+    __syncthreads();  // the list entries written by other lanes are in
+    const int half = lane >> 5;
+    for (int i0 = 0; i0 < nbl; i0 += 8) {
+      int blk[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) blk[u] = i0 + u < nbl ? blist[i0 + u] : -1;
+      int64_t ii[4];
+      bool ok[4];
+      float sv[4], nv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int b = half ? blk[2 * r + 1] : blk[2 * r];
+        ii[r] = static_cast<int64_t>(b) * kKB + (lane & (kKB - 1));
+        ok[r] = b >= 0 && ii[r] < p.M;
+        sv[r] = ok[r] ? sc[ii[r]] : 0.f;
+        nv[r] = ok[r] ? p.rownorm2[ii[r]] : 0.f;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool cand_ok = ok[r] && (exhaustive || static_cast<double>(sv[r]) + err(nv[r]) >= thresh);
+        const uint64_t cmask = __ballot(cand_ok);
+        if (!cmask) continue;
+        if (ncand + 64 > kCand) {
+          early = true;
+          flush();
+        }
+        if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(ii[r]);
+        ncand += __builtin_popcountll(cmask);
+      }
+    }
+    __syncthreads();  // every list entry is read before the list is refilled
+    nbl = 0;
+  };
   // one group of 256 blocks: lane l holds the maxima and norms of blocks
   // kb0 + 64 j + l
-  auto test_group = [&](int kb0, const float (&b4)[4], const float (&n4)[4]) {
-    uint64_t bmask[4];
+  auto add_group = [&](int kb0, const float (&b4)[4], const float (&n4)[4]) {
+    if (nbl > kBList - 256) test_list();
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int kb = kb0 + 64 * j + lane;
       const bool pass = kb < nkb && (exhaustive || static_cast<double>(b4[j]) + err(n4[j]) >= thresh);
-      bmask[j] = __ballot(pass);
-    }
-    // keys of the surviving blocks, eight blocks per round (two per 64-lane
-    // pass) so their score and norm loads are in flight together
-    const int half = lane >> 5;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint64_t m = bmask[j];
-      while (m) {
-        int blk[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          blk[u] = m ? kb0 + 64 * j + __builtin_ctzll(m) : -1;
-          m &= m - 1;
-        }
-        int64_t ii[4];
-        bool ok[4];
-        float sv[4], nv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int b = half ? blk[2 * r + 1] : blk[2 * r];
-          ii[r] = static_cast<int64_t>(b) * kKB + (lane & (kKB - 1));
-          ok[r] = b >= 0 && ii[r] < p.M;
-          sv[r] = ok[r] ? sc[ii[r]] : 0.f;
-          nv[r] = ok[r] ? p.rownorm2[ii[r]] : 0.f;
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bool cand_ok = ok[r] && (exhaustive || static_cast<double>(sv[r]) + err(nv[r]) >= thresh);
-          const uint64_t cmask = __ballot(cand_ok);
-          if (!cmask) continue;
-          if (ncand + 64 > kCand) {
-            early = true;
-            flush();
-          }
-          if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(ii[r]);
-          ncand += __builtin_popcountll(cmask);
-        }
-      }
+      const uint64_t bmask = __ballot(pass);
+      if (pass) blist[nbl + __builtin_popcountll(bmask & ((1ull << lane) - 1))] = kb;
+      nbl += __builtin_popcountll(bmask);
     }
   };
 #pragma unroll
@@ -689,7 +695,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     if (256 * g < nkb) {
       const float b4[4] = {cb[4 * g], cb[4 * g + 1], cb[4 * g + 2], cb[4 * g + 3]};
       const float n4[4] = {cn[4 * g], cn[4 * g + 1], cn[4 * g + 2], cn[4 * g + 3]};
-      test_group(256 * g, b4, n4);
+      add_group(256 * g, b4, n4);
     }
   }
   for (int kb0 = 256 * kCacheGroups; kb0 < nkb; kb0 += 256) {
@@ -700,8 +706,9 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
       b4[j] = kb < nkb ? bm[kb] : -INFINITY;
       n4[j] = kb < nkb ? p.blocknorm2[kb] : 0.f;
     }
-    test_group(kb0, b4, n4);
+    add_group(kb0, b4, n4);
   }
+  if (nbl > 0) test_list();
   // Top-1 without scores: the candidate list provably holds the exact
   // argmax, so a single candidate is the answer.  With several, each is
   // scored by a lane-parallel fp64 sum (every product exact; each lane sums
