@@ -414,7 +414,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   const int E = static_cast<int>(p.E);
   const int nkb = p.nkb;
   const int k = p.k;
-  __shared__ __attribute__((aligned(16))) float qs[kMaxE];
+  __shared__ __attribute__((aligned(16))) double qs[kMaxE];  // the query in fp64 (exact)
   __shared__ __attribute__((aligned(16))) float rs[kRowWords];
   __shared__ int cand[kCand];
   __shared__ int blist[kBList];
@@ -452,7 +452,10 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int e4 = g0 + 64 * u + lane;
-      if (e4 < e4n) *reinterpret_cast<float4*>(qs + 4 * e4) = v[u];
+      if (e4 < e4n) {
+        reinterpret_cast<double2*>(qs + 4 * e4)[0] = make_double2(v[u].x, v[u].y);
+        reinterpret_cast<double2*>(qs + 4 * e4)[1] = make_double2(v[u].z, v[u].w);
+      }
       nq = fmaf(v[u].x, v[u].x, fmaf(v[u].y, v[u].y, fmaf(v[u].z, v[u].z, fmaf(v[u].w, v[u].w, nq))));
     }
   }
@@ -616,20 +619,23 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     for (int c0 = 0; c0 < ncand; c0 += batch_max) {
       const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
       stage_rows(c0, nb);
-      // the chain stays one fma per feature in feature order; reading four
-      // features per 16-byte LDS access (the query's a broadcast) and
+      // the chain stays one fma per feature in feature order; the query is
+      // held in fp64 (converted once, exactly), so a feature costs one
+      // conversion of the key value and the fma; reading four key values
+      // per 16-byte LDS access (the query's two 16-byte broadcasts) and
       // unrolling lets the reads run ahead of the dependent fp64 chain
       double s = 0.0;
       if (lane < nb) {
         const float* row = rs + lane * pitch;
 #pragma unroll 4
         for (int e = 0; e < E; e += 4) {
-          const float4 qv = *reinterpret_cast<const float4*>(qs + e);
+          const double2 q01 = *reinterpret_cast<const double2*>(qs + e);
+          const double2 q23 = *reinterpret_cast<const double2*>(qs + e + 2);
           const float4 rv = *reinterpret_cast<const float4*>(row + e);
-          s = fma(static_cast<double>(qv.x), static_cast<double>(rv.x), s);
-          s = fma(static_cast<double>(qv.y), static_cast<double>(rv.y), s);
-          s = fma(static_cast<double>(qv.z), static_cast<double>(rv.z), s);
-          s = fma(static_cast<double>(qv.w), static_cast<double>(rv.w), s);
+          s = fma(q01.x, static_cast<double>(rv.x), s);
+          s = fma(q01.y, static_cast<double>(rv.y), s);
+          s = fma(q23.x, static_cast<double>(rv.z), s);
+          s = fma(q23.y, static_cast<double>(rv.w), s);
         }
       }
       merge(s, lane < nb ? cand[c0 + lane] : -1, nb);
@@ -736,7 +742,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
           const float* row = rs + r * pitch;
           double part = 0.0;
           for (int e = lane; e < E; e += 64)
-            part = fma(static_cast<double>(qs[e]), static_cast<double>(row[e]), part);
+            part = fma(qs[e], static_cast<double>(row[e]), part);
           const double a = wave_sum_d(part);
           const int ci = cand[c0 + r];
           const double mu = gs * qn * sqrt(static_cast<double>(p.rownorm2[ci])) + 1e-300;
