@@ -114,6 +114,34 @@ def test_retrieval_norms_past_the_screen_range():
     assert np.array_equal(_gpu_top1(q, K3), ref)
 
 
+def _clustered(Q, M, E, spread, seed):
+    """Unit keys and queries around one direction: the smaller `spread`,
+    the more 32-key blocks come within the screen's error bound of the best."""
+    g = np.random.default_rng(seed)
+    base = g.standard_normal(E)
+    K = base[None, :] + spread * g.standard_normal((M, E))
+    K = (K / np.linalg.norm(K, axis=1, keepdims=True)).astype(np.float32)
+    q = base[None, :] + 0.3 * g.standard_normal((Q, E))
+    q = (q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32)
+    return torch.from_numpy(q), torch.from_numpy(K)
+
+
+@pytest.mark.parametrize("spread", [1e-3, 3e-2])
+def test_retrieval_survivors_past_the_register_groups(spread):
+    """40,000 keys = 1,250 blocks, past the 512 whose maxima the decide wave
+    holds in registers, with many blocks surviving the block test (all of
+    them at spread 1e-3, where every key is a candidate and the candidate
+    list is scored in many batches; some at 3e-2); then the same index with
+    one key of norm 1000 (every key scored exactly)."""
+    q, K = _clustered(8, 40000, 64, spread, 65)
+    ref, _ = oracle.top1(q, K)
+    assert np.array_equal(_gpu_top1(q, K), ref)
+    K2 = K.clone()
+    K2[12345] *= 1000.0
+    ref, _ = oracle.top1(q, K2)
+    assert np.array_equal(_gpu_top1(q, K2), ref)
+
+
 def test_retrieval_components_below_fp16_normal_range():
     """Keys and queries with many components far below 2^-22 (subnormal or
     zero once scaled into fp16) and near-ties decided by them."""

@@ -41,6 +41,20 @@ def test_topk_workload_k3():
     assert np.array_equal(got_i[pos.numpy(), 0], rows.numpy().astype(np.int32))
 
 
+@pytest.mark.parametrize("spread", [1e-3, 3e-2])
+def test_topk_survivors_past_the_register_groups(spread):
+    """Top-3 with scores over 40,000 clustered keys (1,250 blocks, many or
+    all of them surviving the block test): indices and fp64 scores equal the
+    oracle's bit for bit."""
+    g = np.random.default_rng(66)
+    base = g.standard_normal(64)
+    K = base[None, :] + spread * g.standard_normal((40000, 64))
+    K = torch.from_numpy((K / np.linalg.norm(K, axis=1, keepdims=True)).astype(np.float32))
+    q = base[None, :] + 0.3 * g.standard_normal((8, 64))
+    q = torch.from_numpy((q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32))
+    _check_topk(q, K, 3)
+
+
 @pytest.mark.parametrize("Q,M,E,k", [(1, 1, 4, 1), (3, 33, 16, 2), (65, 1000, 20, 5),
                                      (70, 97, 388, 64), (130, 300, 64, 7), (5, 64, 8, 64)])
 def test_topk_ragged_shapes(Q, M, E, k):
