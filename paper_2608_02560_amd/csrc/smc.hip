@@ -5,9 +5,12 @@
 // Routing is exact: every score is the fp64 sum of the exact products of two
 // fp32 values, summed in feature order (one fused multiply-add per term,
 // which rounds exactly as multiply-then-add here), and the argmax keeps the
-// lowest index among equal scores.  One wave per chunk embedding; lane m
-// scores prototype m sequentially.  The work is a few thousand fused
-// multiply-adds per chunk, so the kernel is latency-bound by design.
+// lowest index among equal scores.  One wave per chunk embedding.  Each
+// stage first orders its prototypes by lane-parallel fp64 sums with a proven
+// error bound, which decides the argmax unless two scores lie within the
+// bound of each other; then lane m scores prototype m sequentially, the sum
+// of the definition itself.  The work is a few thousand fused multiply-adds
+// per chunk, so the kernel is latency-bound by design.
 //
 // Consolidation applies s <- (1 - alpha) s + alpha h to the routed semantic
 // state for every chunk in chunk order; rows and element slices run in
@@ -15,11 +18,13 @@
 #include <type_traits>
 
 #include "precog_kernels.h"
+#include "wave_ops.h"
 
 namespace precog {
 namespace {
 
 constexpr int kMaxE = 4096;
+constexpr int kRowFloats = 8192;  // LDS floats for staged prototype rows
 
 __device__ __forceinline__ double shfl_d(double v, int src_lane) {
   const int lo = __builtin_amdgcn_ds_bpermute(src_lane * 4, static_cast<int>(__double2loint(v)));
@@ -62,6 +67,70 @@ __device__ __forceinline__ int wave_argmax(double s, int lane, int n) {
   return bi;
 }
 
+// One routing stage over the n prototype rows at `rows` (row stride E),
+// decided without the sequential sums when that is provably safe: the index
+// of the best (score, lowest index), or -1.  Each row's score is summed
+// lane-parallel in fp64 (every product exact; lane l sums features l, l + 64,
+// ... in order, then the 6-level wave tree), which differs from the exact
+// real sum by at most gamma_{E/64+7} T, T = sum_e |x_e w_e| (summed the same
+// way; the factor 1.01 covers its rounding); the sequential sum of the
+// definition differs from the exact sum by at most gamma_E T.  If the best
+// row's lower end beats every other row's upper end, that row is also the
+// sequential argmax.  Otherwise (near or exact ties, NaN or infinite
+// values) the caller scores the stage sequentially.  Rows are staged through
+// LDS a batch at a time (fixed-width groups of predicated 16-byte loads, so
+// a batch's loads are in flight together).
+__device__ int fast_stage(const float* ex, float* rs, const float* rows, int n, int E, int lane) {
+  const double u53 = 1.1102230246251565e-16;  // 2^-53
+  const double dp = static_cast<double>(E / 64 + 7);
+  const double en = static_cast<double>(E);
+  const double gs = 1.01 * (dp * u53 / (1.0 - dp * u53) + en * u53 / (1.0 - en * u53));
+  const int per = kRowFloats / E < 8 ? kRowFloats / E : 8;
+  double best = 0.0, best_mu = 0.0, others = -INFINITY;
+  int bi = -1;
+  bool bad = false;
+  for (int m0 = 0; m0 < n; m0 += per) {
+    const int nb = n - m0 < per ? n - m0 : per;
+    const int tot = nb * (E / 4);
+    const float4* src = reinterpret_cast<const float4*>(rows + static_cast<int64_t>(m0) * E);
+    __syncthreads();  // the previous batch is consumed
+    for (int f0 = 0; f0 < tot; f0 += 8 * 64) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int f = f0 + 64 * u + lane;
+        v[u] = f < tot ? src[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int f = f0 + 64 * u + lane;
+        if (f < tot) reinterpret_cast<float4*>(rs)[f] = v[u];
+      }
+    }
+    __syncthreads();
+    for (int r = 0; r < nb; ++r) {
+      double part = 0.0, apart = 0.0;
+      for (int e = lane; e < E; e += 64) {
+        const double pr = static_cast<double>(ex[e]) * static_cast<double>(rs[r * E + e]);
+        part += pr;
+        apart += fabs(pr);
+      }
+      const double a = wave_sum_d(part);
+      const double mu = gs * wave_sum_d(apart) + 1e-300;
+      if (!(a == a) || !(mu < INFINITY)) bad = true;
+      if (bi < 0 || a > best) {
+        if (bi >= 0) others = fmax(others, best + best_mu);
+        best = a;
+        best_mu = mu;
+        bi = m0 + r;
+      } else {
+        others = fmax(others, a + mu);
+      }
+    }
+  }
+  return !bad && best - best_mu > others ? bi : -1;
+}
+
 __global__ __launch_bounds__(64) void route_kernel(const RouteParams p) {
   const int64_t c = blockIdx.x;
   const int lane = threadIdx.x;
@@ -70,14 +139,24 @@ __global__ __launch_bounds__(64) void route_kernel(const RouteParams p) {
   const float4* src = reinterpret_cast<const float4*>(p.emb + c * p.E);
   for (int i = lane; i < E / 4; i += 64) e4[i] = src[i];
   __syncthreads();
-  // stage 1: domain m* = argmax_m <phi(c), p_m>
-  double s = 0.0;
-  if (lane < p.ndom) s = exact_dot(e4, p.dom + static_cast<int64_t>(lane) * p.E, E);
-  const int m = wave_argmax(s, lane, p.ndom);
+  __shared__ float rs[kRowFloats];
+  const float* ex = reinterpret_cast<const float*>(e4);
+  // stage 1: domain m* = argmax_m <phi(c), p_m>; lane m scores prototype m
+  // sequentially when the fast ordering cannot decide
+  int m = fast_stage(ex, rs, p.dom, p.ndom, E, lane);
+  if (m < 0) {
+    double s = 0.0;
+    if (lane < p.ndom) s = exact_dot(e4, p.dom + static_cast<int64_t>(lane) * p.E, E);
+    m = wave_argmax(s, lane, p.ndom);
+  }
   // stage 2: sub-cluster j* = argmax_j <phi(c), q_{m*, j}>
-  s = 0.0;
-  if (lane < p.nsub) s = exact_dot(e4, p.sub + (static_cast<int64_t>(m) * p.nsub + lane) * p.E, E);
-  const int j = wave_argmax(s, lane, p.nsub);
+  const float* subs = p.sub + static_cast<int64_t>(m) * p.nsub * p.E;
+  int j = fast_stage(ex, rs, subs, p.nsub, E, lane);
+  if (j < 0) {
+    double s = 0.0;
+    if (lane < p.nsub) s = exact_dot(e4, subs + static_cast<int64_t>(lane) * p.E, E);
+    j = wave_argmax(s, lane, p.nsub);
+  }
   if (lane == 0) {
     p.dom_out[c] = m;
     p.sub_out[c] = j;

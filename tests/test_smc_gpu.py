@@ -34,7 +34,7 @@ def test_route_workload_bit_exact():
 
 
 @pytest.mark.parametrize("C,E,nd,ns", [(1, 4, 1, 1), (7, 20, 64, 3), (33, 388, 5, 64),
-                                       (300, 384, 8, 8)])
+                                       (300, 384, 8, 8), (3, 4096, 9, 5), (5, 4, 64, 64)])
 def test_route_random_shapes(C, E, nd, ns):
     g = np.random.default_rng(C + E)
     emb = torch.from_numpy(synth.unit_rows_host(C, E, g))
