@@ -95,6 +95,42 @@ def test_route_equal_real_scores_decided_by_summation_order():
     assert all(outs)
 
 
+def test_route_near_ties_one_ulp_apart():
+    """Domain and sub-cluster prototypes that differ from the winning one in
+    a single component by one fp32 ulp, up or down: real scores a hair apart,
+    above the lane-parallel sums' error bound (decided by them) or, where the
+    embedding's component is 1e-30, far below it (decided by the sequential
+    fp64 sums), either way exactly as the definition orders them."""
+    g = np.random.default_rng(68)
+    C, E, nd, ns = 48, 384, 6, 4
+    emb = synth.unit_rows_host(C, E, g)
+    for i in range(C):
+        dom = synth.unit_rows_host(nd, E, g)
+        sub = synth.unit_rows_host(nd * ns, E, g).reshape(nd, ns, E)
+        rm, _ = oracle.route2(emb[i:i + 1], dom, sub)
+        w = int(rm[0])
+        c = int(g.integers(0, E))
+        up = bool(i % 2)
+        if i % 4 >= 2:
+            # the embedding's component there is tiny: the real scores differ
+            # far below the error bound, so the sequential sums decide (equal
+            # sums go to the lower index)
+            emb[i, c] = np.float32(1e-30)
+            rm, _ = oracle.route2(emb[i:i + 1], dom, sub)
+            w = int(rm[0])
+        twin = dom[w].copy()
+        twin[c] = np.nextafter(twin[c], np.float32(np.inf) if up else np.float32(-np.inf))
+        dom[(w + 1 + i % (nd - 1)) % nd] = twin
+        rm, rj = oracle.route2(emb[i:i + 1], dom, sub)
+        wm, sw = int(rm[0]), int(rj[0])
+        st = sub[wm, sw].copy()
+        st[c] = np.nextafter(st[c], np.float32(-np.inf) if up else np.float32(np.inf))
+        sub[wm, (sw + 1) % ns] = st
+        rm, rj = oracle.route2(emb[i:i + 1], dom, sub)
+        m, j, _ = _route(*(torch.from_numpy(np.ascontiguousarray(x)) for x in (emb[i:i + 1], dom, sub)))
+        assert m[0] == rm[0] and j[0] == rj[0], (i, m[0], rm[0], j[0], rj[0])
+
+
 def _cons_bound(states0, contrib, target, alpha, mag_unit):
     """Per-row bound: each fp32 update adds at most 3 units of 2^-24 of the
     magnitudes involved (two roundings of the factors, one of the fused
