@@ -84,6 +84,29 @@ def test_retrieval_equal_real_scores_decided_by_summation_order():
     assert np.array_equal(_gpu_top1(torch.from_numpy(qn), torch.from_numpy(Kn)), ref)
 
 
+def test_retrieval_near_ties_one_ulp_apart():
+    """A twin of each query's winner with one component moved by one fp32
+    ulp, up or down: both reach the exact rescoring; the real gap is above
+    the lane-parallel ordering's error bound (decided by it) or, where the
+    query's component is 1e-30, far below it (decided by the sequential fp64
+    sums, equal sums going to the lower index)."""
+    g = np.random.default_rng(69)
+    q, K, _, _ = synth.retrieval_inputs_host(48, 2000, 384, 0, seed=69)
+    qn, Kn = q.numpy().copy(), K.numpy().copy()
+    cs = [int(v) for v in g.integers(0, 384, 48)]
+    for i in range(48):
+        if i % 4 >= 2:
+            qn[i, cs[i]] = np.float32(1e-30)
+    win, _ = oracle.top1(qn, Kn)
+    for i, w in enumerate(win):
+        twin = Kn[w].copy()
+        c = cs[i]
+        twin[c] = np.nextafter(twin[c], np.float32(np.inf) if i % 2 else np.float32(-np.inf))
+        Kn[(w + 1 + 37 * i) % 2000] = twin
+    ref, _ = oracle.top1(qn, Kn)
+    assert np.array_equal(_gpu_top1(torch.from_numpy(qn), torch.from_numpy(Kn)), ref)
+
+
 def test_retrieval_non_unit_rows_and_empty():
     q, K, _, _ = synth.retrieval_inputs_host(40, 500, 64, 8, seed=62)
     scale = torch.from_numpy(np.random.default_rng(1).uniform(0.1, 30.0, (500, 1))).float()
