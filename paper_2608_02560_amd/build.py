@@ -30,37 +30,33 @@ DEVICE = ["-x", "hip", "--offload-arch=" + ARCH,
           "-munsafe-fp-atomics"]
 
 
-def _compile(src: str, build_dir: str = BUILD, defines=()) -> str:
-    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+def _compile(src: str) -> str:
+    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     cmd = [HIPCC] + COMMON + (DEVICE if src.endswith(".hip") else
-                              ["--offload-arch=" + ARCH]) + ["-D" + d for d in defines] + \
-        ["-c", src, "-o", obj]
+                              ["--offload-arch=" + ARCH]) + ["-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), res.stderr))
     return obj
 
 
-def build(jobs: int | None = None, verbose: bool = False, out: str = LIB, defines=()) -> str:
-    """Compile every source under csrc/ and link libprecog.so; returns its path.
-    `out` and `defines` (NAME=VALUE preprocessor definitions) build a variant
-    of the library elsewhere, e.g. for tuning constants."""
-    build_dir = BUILD if out == LIB else out + ".objs"
-    os.makedirs(build_dir, exist_ok=True)
+def build(jobs: int | None = None, verbose: bool = False) -> str:
+    """Compile every source under csrc/ and link libprecog.so; returns its path."""
+    os.makedirs(BUILD, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) +
                   glob.glob(os.path.join(CSRC, "*.cpp")))
     jobs = jobs or min(8, len(srcs))
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, build_dir, defines), srcs))
-    tmp = out + ".tmp%d" % os.getpid()
+        objs = list(ex.map(_compile, srcs))
+    tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (" ".join(cmd), res.stderr))
-    os.replace(tmp, out)
+    os.replace(tmp, LIB)
     if verbose:
-        print("built", out)
-    return out
+        print("built", LIB)
+    return LIB
 
 
 if __name__ == "__main__":

@@ -54,9 +54,11 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t auto_chunk(const precog_scan_desc* d);
 
 // Longest chunk whose per-token streams stay addressable with the kernels'
-// 32-bit buffer offsets: chunk * D * 4 bytes (the widest element) < 2^31.
+// 32-bit buffer offsets: x, dt, z, y take D elements per token and B, C take
+// N, at most 4 bytes each, so chunk * max(D, N) * 4 < 2^31.
 int64_t max_chunk(const precog_scan_desc* d) {
-  const int64_t row = (d->dim > 0 ? d->dim : 1) * 4;
+  const int64_t w = d->dim > d->dstate ? d->dim : d->dstate;
+  const int64_t row = (w > 0 ? w : 1) * 4;
   return ((1LL << 31) - 1) / row;
 }
 

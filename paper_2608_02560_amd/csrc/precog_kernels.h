@@ -52,10 +52,7 @@ struct ScanParams {
 // Threads per workgroup of the real-A scan kernels: 8 waves, so that the two
 // waves sharing a SIMD at two waves per SIMD belong to one workgroup and can
 // see each other's progress in LDS (see scan_kernels.h).
-#ifndef PRECOG_SCAN_WG
-#define PRECOG_SCAN_WG 512
-#endif
-constexpr int kScanThreads = PRECOG_SCAN_WG;
+constexpr int kScanThreads = 512;
 
 // Launchers (return the HIP launch status).  in/out/state dtypes are the
 // precog_dtype codes of the public header.

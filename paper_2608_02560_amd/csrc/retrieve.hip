@@ -51,10 +51,7 @@ constexpr int kQW = 32;       // queries per wave (one 32 x 32 tile)
 constexpr int kQWG = 4 * kQW; // queries per workgroup
 // features per chunk: the wave preloads its query operands for a whole chunk
 // (kFC / 16 x 4 VGPRs)
-#ifndef PRECOG_RET_FC
-#define PRECOG_RET_FC 128
-#endif
-constexpr int kFC = PRECOG_RET_FC;
+constexpr int kFC = 128;
 constexpr int kKS = kFC / 16; // 16-feature MFMA steps per chunk
 
 __device__ __forceinline__ float xor_shfl(float v, int m) {

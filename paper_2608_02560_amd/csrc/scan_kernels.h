@@ -48,11 +48,6 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kSBlock = kScanThreads;    // scan workgroups (real and complex A): 8 waves
 
-// Progress balancing between the waves of a workgroup that share a SIMD
-// (see scan_kernel).
-#ifndef PRECOG_SCAN_FAIR
-#define PRECOG_SCAN_FAIR 1
-#endif
 constexpr int kSWaves = kSBlock / 64;
 
 // Progress balancing (launches whose waves are all resident at once; the
@@ -67,7 +62,7 @@ constexpr int kSWaves = kSBlock / 64;
 // stay at 0; their live partners then run at priority 0, which changes
 // nothing.)
 __device__ __forceinline__ bool balance_enabled(const ScanParams& p) {
-  return PRECOG_SCAN_FAIR != 0 && kSWaves == 8 && (p.flags & kBalance) != 0;
+  return kSWaves == 8 && (p.flags & kBalance) != 0;
 }
 // Before any wave of the workgroup can leave: every wave starts at 0.
 __device__ __forceinline__ void balance_init(int* progress, int wave) {
@@ -90,20 +85,11 @@ __device__ __forceinline__ void balance_step(int* progress, int wave, int tile) 
 // SIMD either way).  Trajectory capture keeps 8: its state stores share the
 // vector-memory counter with the tile loads, and longer tiles wait on them
 // less often.
-#ifndef PRECOG_SCAN_PF
-#define PRECOG_SCAN_PF 4
-#endif
-constexpr int kPFPlain = PRECOG_SCAN_PF;
+constexpr int kPFPlain = 4;
 constexpr int kPFWide = 8;  // trajectory capture, complex-A kernel
 
 enum Kind { kReadout = 0, kStateOnly = 1, kSummary = 2 };
 
-// B_t and C_t reach the lanes through LDS (1) or DPP row broadcasts (0); see
-// the kernel.
-#ifndef PRECOG_SCAN_LDS_BCAST
-#define PRECOG_SCAN_LDS_BCAST 1
-#endif
-constexpr bool kLdsBcast = PRECOG_SCAN_LDS_BCAST != 0;
 
 
 __device__ __forceinline__ float to_f32(float v) { return v; }
@@ -529,7 +515,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // token replaced), or when a channel spans several lanes (N > 16); a
   // readout-free N = 16 scan saves only the 16 B broadcasts, less than the
   // staging costs.
-  constexpr bool kLds = kLdsBcast && NL == 16 && (kRead || P > 1);
+  constexpr bool kLds = NL == 16 && (kRead || P > 1);
   __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kSBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
   // bf16 coefficients go in as raw bits into the high half of a word whose
   // low half is zero (cleared once, below): the word is then the exact fp32

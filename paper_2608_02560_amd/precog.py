@@ -13,9 +13,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# PRECOG_LIBRARY selects another build of the same library (e.g. a tuning
-# variant); by default the in-tree build is loaded.
-LIB_PATH = os.environ.get("PRECOG_LIBRARY") or os.path.join(_HERE, "libprecog.so")
+# Always the in-tree build: tests, smoke and bench measure the library built
+# from this tree's sources.
+LIB_PATH = os.path.join(_HERE, "libprecog.so")
 
 F32, BF16, F16 = 0, 1, 2
 _DT = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}

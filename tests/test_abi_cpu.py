@@ -121,6 +121,24 @@ def test_scan_workspace_sizes():
     assert P.scan_workspace_bytes(P.scan_desc(2, 100, 60, 16)) == 0
 
 
+def test_chunk_cap_covers_the_coefficient_streams():
+    """Chunks are capped so every per-token stream stays addressable with
+    32-bit buffer offsets: chunk * max(D, N) * 4 < 2^31.  With D = 8 and
+    N = 64 the coefficient rows B_t, C_t are the wider ones, so a one-chunk
+    request over 3 * 2^23 tokens is cut into 4 chunks (the cap is
+    (2^31 - 1) / 256 = 2^23 - 1 tokens), which shows in the carry workspace."""
+    L = 3 * (1 << 23)
+    d = P.scan_desc(1, L, 8, 64, chunk=L)
+    nch = -(-L // ((2 ** 31 - 1) // (64 * 4)))
+    assert nch == 4
+    carry = nch * 8 * 64 * 4
+    dts = -(-(nch * 8 * 4) // 256) * 256
+    assert P.scan_workspace_bytes(d) == carry + dts
+    # D wider than N: the cap follows D, (2^31 - 1) / (512 * 4) = 2^20 - 1 tokens
+    assert P.scan_workspace_bytes(P.scan_desc(1, (1 << 20) - 1, 512, 16, chunk=1 << 20)) == 0
+    assert P.scan_workspace_bytes(P.scan_desc(1, 1 << 20, 512, 16, chunk=1 << 20)) > 0
+
+
 def test_retrieve_validation_errors():
     L = P.lib()
     ws = P.retrieve_workspace_bytes(4, 10, 16)
