@@ -12,6 +12,8 @@
  *                           captured hT (Eq. 1, Sec. 3; capture, Sec. 4.2)
  *   precog_retrieve_top1    exact cosine top-1 over a key index (Sec. 4.2)
  *   precog_inject_gather    h0[q] <- store[idx[q]] (Sec. 4.2, query time)
+ * for callers that cannot allocate device memory:
+ *   precog_retrieve_top1_noalloc  top-1 with a fixed library-held workspace
  * with the injection fused into the query prefill:
  *   precog_scan_encode_indexed  the scan starting from store[idx] rows or
  *                           their top-k softmax composition
@@ -37,7 +39,8 @@
  *     validation failure nothing is written and the status says why.  A HIP
  *     launch failure returns PRECOG_ERR_HIP.  No C++ exception crosses the
  *     ABI.  The only library state is a per-device cache of the architecture
- *     check.
+ *     check and, for precog_retrieve_top1_noalloc, a fixed device array per
+ *     device with its looked-up address.
  *   - Layouts are row-major with the last index fastest.
  *   - Entry points may be called concurrently from several host threads on
  *     different streams; calls on one stream execute in order.
@@ -260,6 +263,29 @@ precog_status precog_retrieve_top1(const float *query_emb,
  *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
  *   workspace precog_retrieve_workspace_bytes(Q, M, E) bytes (the same as
  *             for top-1).  Non-finite inputs give unspecified indices. */
+/* Bytes of the device array behind precog_retrieve_top1_noalloc: 32 MiB,
+ * held on each device the library runs on until the process ends. */
+#define PRECOG_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* precog_retrieve_top1 for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments (minus the workspace), same result, bit for
+ * bit; its workspace is a fixed array of PRECOG_NOALLOC_SCRATCH_BYTES in
+ * this library's device memory, one per device.  The call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine); its first
+ * call on a device looks up that device's copy of the array.
+ *   Limit: precog_retrieve_workspace_bytes(Q, M, E) must not exceed
+ *   PRECOG_NOALLOC_SCRATCH_BYTES (about Q * M <= 8.3e6 pairs), else
+ *   PRECOG_ERR_WORKSPACE and nothing is enqueued.
+ *   Every call on one device shares that device's array: calls that overlap
+ *   on one device (different streams without ordering between them, or
+ *   several host threads) race and give unspecified indices.  Calls ordered
+ *   on one stream are safe; nothing carries over from one call to the next. */
+precog_status precog_retrieve_top1_noalloc(const float *query_emb,
+                                           const float *index_emb, int64_t Q,
+                                           int64_t M, int64_t E, int32_t *idx,
+                                           void *stream);
+
 precog_status precog_retrieve_topk(const float *query_emb,
                                    const float *index_emb, int64_t Q, int64_t M,
                                    int64_t E, int64_t k, int32_t *idx,

@@ -312,6 +312,8 @@ RetrieveWs retrieve_ws(int64_t Q, int64_t M, int64_t E) {
 
 size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096 || E % 4 != 0) return 0;
+  if (Q > 0x7fffffffLL || M > 0x7fffffffLL || ceil_div(M, 32) * ceil_div(Q, 128) > 0x7fffffffLL)
+    return 0;
   return retrieve_ws(Q, M, E).total;
 }
 
@@ -365,10 +367,13 @@ precog_status precog_retrieve_prepare(const float* index_emb, int64_t M, int64_t
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 
-namespace {
-precog_status retrieve(const float* query_emb, const float* index_emb, const void* prepared,
-                       int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx, double* score,
-                       void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace precog {
+precog_status retrieve_entry(const float* query_emb, const float* index_emb, const void* prepared,
+                             int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
+                             double* score, void* workspace, size_t workspace_bytes,
+                             void* stream) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
@@ -423,12 +428,14 @@ precog_status retrieve(const float* query_emb, const float* index_emb, const voi
   const hipError_t e = precog::launch_retrieve(p, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
-}  // namespace
+}  // namespace precog
+
+extern "C" {
 
 precog_status precog_retrieve_top1(const float* query_emb, const float* index_emb, int64_t Q,
                                    int64_t M, int64_t E, int32_t* idx, void* workspace,
                                    size_t workspace_bytes, void* stream) {
-  return retrieve(query_emb, index_emb, nullptr, Q, M, E, 1, idx, nullptr, workspace,
+  return precog::retrieve_entry(query_emb, index_emb, nullptr, Q, M, E, 1, idx, nullptr, workspace,
                   workspace_bytes, stream);
 }
 
@@ -436,7 +443,7 @@ precog_status precog_retrieve_topk(const float* query_emb, const float* index_em
                                    int64_t M, int64_t E, int64_t k, int32_t* idx, double* score,
                                    void* workspace, size_t workspace_bytes, void* stream) {
   if (k < 1 || k > precog::kMaxTopK || k > M) return PRECOG_ERR_SHAPE;
-  return retrieve(query_emb, index_emb, nullptr, Q, M, E, k, idx, score, workspace,
+  return precog::retrieve_entry(query_emb, index_emb, nullptr, Q, M, E, k, idx, score, workspace,
                   workspace_bytes, stream);
 }
 
@@ -448,7 +455,7 @@ precog_status precog_retrieve_topk_prepared(const float* query_emb, const float*
   if (k < 1 || k > precog::kMaxTopK || k > M) return PRECOG_ERR_SHAPE;
   if (!prepared) return PRECOG_ERR_NULL;
   if (prepared_bytes < precog_retrieve_index_bytes(M, E)) return PRECOG_ERR_WORKSPACE;
-  return retrieve(query_emb, index_emb, prepared, Q, M, E, k, idx, score, workspace,
+  return precog::retrieve_entry(query_emb, index_emb, prepared, Q, M, E, k, idx, score, workspace,
                   workspace_bytes, stream);
 }
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "precog.h"
+
 namespace precog {
 
 // Storage tags.  bf16 and fp16 are both 16-bit; the tags keep them apart.
@@ -84,6 +86,12 @@ struct RetrieveParams {
 };
 constexpr int kMaxTopK = 64;
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
+// Body of the retrieval entry points (precog_abi.cpp): validates the
+// arguments, lays out `workspace` and launches; `prepared` may be null.
+precog_status retrieve_entry(const float* query_emb, const float* index_emb, const void* prepared,
+                             int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
+                             double* score, void* workspace, size_t workspace_bytes,
+                             void* stream);
 // Prepared index: p.kop, p.rownorm2 and p.blocknorm2 are written from p.K.
 hipError_t launch_retrieve_prepare(const RetrieveParams& p, hipStream_t s);
 

@@ -28,6 +28,7 @@ EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_enc
            "precog_scan_trajectory",
            "precog_scan_complex",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
+           "precog_retrieve_top1_noalloc",
            "precog_retrieve_topk", "precog_retrieve_index_bytes", "precog_retrieve_prepare",
            "precog_retrieve_topk_prepared", "precog_inject_gather", "precog_inject_compose",
            "precog_smc_route", "precog_smc_consolidate", "precog_status_string")
@@ -77,6 +78,8 @@ def lib():
         L.precog_retrieve_workspace_bytes.restype = sz
         L.precog_retrieve_top1.argtypes = [vp, vp, i64, i64, i64, vp, vp, sz, vp]
         L.precog_retrieve_top1.restype = ctypes.c_int
+        L.precog_retrieve_top1_noalloc.argtypes = [vp, vp, i64, i64, i64, vp, vp]
+        L.precog_retrieve_top1_noalloc.restype = ctypes.c_int
         L.precog_retrieve_topk.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, sz, vp]
         L.precog_retrieve_topk.restype = ctypes.c_int
         L.precog_retrieve_index_bytes.argtypes = [i64, i64]
@@ -190,6 +193,19 @@ def retrieve_top1(query, index, idx, workspace, workspace_bytes=None, stream=Non
     st = lib().precog_retrieve_top1(_ptr(query), _ptr(index), Q, M, E, _ptr(idx),
                                     _ptr(workspace), int(workspace_bytes), _stream(stream))
     _check("precog_retrieve_top1", st)
+
+
+def retrieve_top1_noalloc(query, index, idx, stream=None):
+    """precog_retrieve_top1_noalloc: top-1 with the library's fixed device
+    array as workspace (nothing allocated)."""
+    Q, E = query.shape
+    M = index.shape[0]
+    st = lib().precog_retrieve_top1_noalloc(_ptr(query), _ptr(index), Q, M, E, _ptr(idx),
+                                            _stream(stream))
+    _check("precog_retrieve_top1_noalloc", st)
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 def retrieve_topk(query, index, k, idx, score, workspace, workspace_bytes=None, stream=None):
