@@ -1,17 +1,27 @@
 """Benchmark of the PRECOG hot path on one MI355X.
 
-Default workload: corpus-chunk encoding -- 64 chunks x 3000 tokens, D=2048,
+Headline workload: corpus-chunk encoding -- 64 chunks x 3000 tokens, D=2048,
 N=16, bf16 inputs, fp32 state, bf16 y, fp16 captured final states -- the
 offline indexing pass of Sec. 4.2.  One step = one precog_scan_encode call
 over the whole batch, inputs resident in HBM.  Prints ONE JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--extra]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--quick]
 
---extra also times the query-time path (top-1 retrieval, state injection,
-32-token query prefill; the same with the injection fused into the prefill;
-and its top-3 variant with softmax composition, separate or fused), the
-long-context chunked scan and one layer of the large corpus encode, reported
-under "extra".
+Besides the headline, the default run times the other four workloads, each
+with its algorithmic bytes, GB/s and fraction of HBM peak and with the oracle
+timed beside it on the host cores:
+
+  single_layer   1 x 512 x 128 x 16 fp32, cold and warm, and split at t = 384
+  query_path     top-1 retrieval over 10,000 x 384 keys for 256 queries, the
+                 retrieved state injected into a 32-token bf16 prefill
+                 (injection fused into the scan), cold cache
+  long_context   8 x 65,536 x 2048 x 16 bf16 scanned in 256-token chunks
+  large_corpus   1024 x 3000 x 1536 x 64 bf16 per layer, state-only, all 24
+                 layers timed with per-layer seeded inputs
+
+and the extensions (top-k composition, SMC trajectory / routing /
+consolidation, complex-A scan) under "extensions".  --quick times the
+headline alone.
 """
 from __future__ import annotations
 
@@ -27,32 +37,36 @@ if ROOT not in sys.path:
 
 METRIC = "SSM prefill scan tokens/s & achieved HBM GB/s (fraction of peak), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
-# v_exp_f32 issues at a quarter of the fp32 slot rate: the 157.3 TFLOP/s
-# vector peak is 7.86e13 slots/s x 2 flops, so 1.97e13 exp/s (measured on
-# the box: ~8 cycles per wave64 v_exp_f32 per SIMD at 8 waves, the same)
-EXP_PEAK_PER_S = 157.3e12 / 2 / 4
-# MI355X fp32 vector peak: 157.3 TFLOP/s = 7.86e13 FMA issue slots/s (256 CUs x
-# 2.4 GHz x 128 lanes).  The scan's algorithmic work per (token, channel,
-# state) is 8 issue slots: v_mul (dt A'), v_exp_f32 (quarter rate: 4 slots),
-# v_mul (B x dt), v_fma (state), v_fma (readout); expressed as FMA-equivalent
-# flops (2 per slot) it is 16 per (t, d, n).
+# MI355X fp32 vector peak 157.3 TFLOP/s = 256 CUs x 4 SIMDs x 2.4 GHz x 64
+# flops per cycle, i.e. 7.86e13 fused multiply-add issue slots per second.
 VALU_PEAK_TFLOPS = 157.3
-SLOT_FLOPS_PER_TDN = 16
+SLOT_PEAK_PER_S = VALU_PEAK_TFLOPS * 1e12 / 2
+# v_exp_f32 issues at a quarter of that slot rate: 1.97e13 exp/s (measured on
+# the box: ~8 cycles per wave64 v_exp_f32 per SIMD at 8 waves, the same).
+EXP_PEAK_PER_S = SLOT_PEAK_PER_S / 4
+# Work per (token, channel, state) of the scan: 1 exp2, 1 multiply (dt A'),
+# 1 multiply (u B), 1 FMA (state), 1 FMA (readout) = 6 flops + 1 exp.  As
+# issue slots: 4 for the quarter-rate exp + 4 plain = 8.
+FLOPS_PER_TDN = 6
+SLOTS_PER_TDN = 8
+MFMA_F16_PEAK_TFLOPS = 2500.0
 PROFILE = os.path.join(ROOT, "profiles", "scan_corpus_encode_b64_l3000_d2048_n16.md")
 SCAN_SOURCE = os.path.join(ROOT, "paper_2608_02560_amd", "csrc", "scan_kernels.h")
+HOLD_CYCLES = 1_000_000  # spin length of the stream hold (well above one host enqueue)
 
 
-def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate=True):
+def scan_bytes(B, L, D, N, in_bytes=2, y_bytes=2, st_bytes=2, readout=True, gate=True,
+               h0_bytes=0):
     """Algorithmic bytes of one scan: every input read once, every output
     written once (x, dt, [z] per (t, d); B, [C] per (t, n); y per (t, d);
-    hT per (d, n); A and Dskip per (d, n) / d)."""
+    hT (and h0 when read) per (d, n); A and Dskip per (d, n) / d)."""
     td = B * L * D
     tn = B * L * N
     total = td * in_bytes * (2 + (1 if (readout and gate) else 0))
     total += tn * in_bytes * (2 if readout else 1)
     if readout:
         total += td * y_bytes + D * 4
-    total += B * D * N * st_bytes + D * N * 4
+    total += B * D * N * (st_bytes + h0_bytes) + D * N * 4
     return total
 
 
@@ -80,15 +94,28 @@ def measured_traffic():
         return None
 
 
-def cpu_threads():
+def host_cpus():
+    """(threads used by the oracle, logical CPUs of the host, CPUs this
+    process may run on).  The oracle uses this process's CPUs, at most 16
+    (the CPU share of one GPU on the GPU machine)."""
+    nproc = os.cpu_count() or 1
     try:
-        n = len(os.sched_getaffinity(0))
+        aff = len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(16, n))
+        aff = nproc
+    return max(1, min(16, aff)), nproc, aff
 
 
-HOLD_CYCLES = 1_000_000  # spin length of the stream hold (well above one host enqueue)
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def time_events(fn, reps, flush=None, hold=False):
@@ -117,37 +144,47 @@ def time_events(fn, reps, flush=None, hold=False):
     return total / reps
 
 
-def cpu_baseline_corpus(inp, wl, rows_b):
-    """The oracle, as it stands, on the first rows_b chunks of the workload
-    (all channels, all tokens), timed on the host cores."""
+def log(msg):
+    """Progress of the run, on stderr (stdout carries the one JSON line)."""
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def rates(nbytes, ms):
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    return {"bytes": nbytes, "gbps": gbps, "hbm_frac": gbps / HBM_PEAK_GBPS}
+
+
+def f64_rows(inp, b0, b1, keys=("x", "dt", "z", "B", "C"), L=None):
+    """Batch rows [b0, b1) (first L tokens) of the scan inputs as contiguous
+    fp64 numpy arrays (exact widening), plus A and Dskip."""
+    import numpy as np
+
+    out = {}
+    for k in keys:
+        v = inp.get(k)
+        out[k] = None if v is None else np.ascontiguousarray(
+            v[b0:b1, :L].float().cpu().numpy(), dtype=np.float64)
+    out["A"] = inp["A"].double().cpu().numpy()
+    out["Dskip"] = None if inp.get("Dskip") is None else inp["Dskip"].double().cpu().numpy()
+    return out
+
+
+def oracle_scan_time(inp, b0, b1, L=None, threads=1, want_y=True, h0=None):
+    """Seconds the oracle's scan takes on batch rows [b0, b1) (first L tokens),
+    its inputs widened to fp64 beforehand (outside the timing)."""
     import oracle
 
-    nthr = cpu_threads()
-    sub = {k: (v[:rows_b].cpu() if v is not None and v.dim() == 3 else
-               (v.cpu() if v is not None else None)) for k, v in inp.items()}
+    a = f64_rows(inp, b0, b1, keys=("x", "dt", "z", "B", "C") if want_y else ("x", "dt", "B"),
+                 L=L)
     t0 = time.perf_counter()
-    oracle.scan(sub["x"], sub["dt"], sub["A"], sub["B"], sub["C"], sub["z"], sub["Dskip"],
-                None, nthreads=nthr)
-    dt = time.perf_counter() - t0
-    tokens = rows_b * wl.seqlen
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
-            "sample": "%d of %d chunks x %d tokens x %d channels, N=%d, fp64, %.1f s wall"
-                      % (rows_b, wl.batch, wl.seqlen, wl.dim, wl.dstate, dt),
-            "cpu": cpu_model()}
+    oracle.scan(a["x"], a["dt"], a["A"], a["B"], a.get("C"), a.get("z"), a["Dskip"], h0,
+                want_y=want_y, nthreads=threads)
+    return time.perf_counter() - t0
 
 
-def cpu_model():
-    """The host CPU's model name, from /proc/cpuinfo."""
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
-    except OSError:
-        pass
-    return "unknown"
-
-
+# ----------------------------------------------------------------------------
+# headline: corpus-chunk encoding
+# ----------------------------------------------------------------------------
 def bench_corpus(args):
     import torch
 
@@ -159,7 +196,7 @@ def bench_corpus(args):
     inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, wl.dt_mu, wl.dt_sigma)
     y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
     hT = torch.empty((B, D, N), dtype=torch.float16, device="cuda")
-    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=args.chunk)
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16)
     nws = P.scan_workspace_bytes(desc)
     ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
 
@@ -182,8 +219,9 @@ def bench_corpus(args):
     ms = max(wall * 1e3 / args.steps, ev_ms)
     nbytes = scan_bytes(B, L, D, N)
     tokens = B * L
-    achieved = nbytes / (ev_ms * 1e-3) / 1e9
-    alu = SLOT_FLOPS_PER_TDN * B * L * D * N / (ev_ms * 1e-3) / 1e12
+    tdn = B * L * D * N
+    sec = ev_ms * 1e-3
+    achieved = nbytes / sec / 1e9
     out = {
         "metric": METRIC,
         "value": tokens / (ms * 1e-3),
@@ -199,196 +237,389 @@ def bench_corpus(args):
         "io_dtypes": "x/dt/z/B/C bf16, y bf16, state fp32, hT fp16",
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": B, "seqlen": L, "dim": D, "dstate": N,
-                   "chunk": args.chunk or "auto", "parallelism": "single GPU"},
+                   "chunk": "auto (one pass)", "parallelism": "single GPU"},
         "achieved_gbps": achieved,
         "hbm_frac": achieved / HBM_PEAK_GBPS,
-        "roofline": {"bound": "alu", "achieved": alu, "peak": VALU_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": alu / VALU_PEAK_TFLOPS,
+        # the metric's roofline: algorithmic bytes (each input read once,
+        # each output written once) over the kernel's event-timed duration
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(),
                      "kernel": "scan_kernel<16, bf16, bf16, fp16, readout, gate>",
-                     "kernel_ms": ev_ms,
-                     "work": "16 FMA-equivalent flops (8 fp32 issue slots) per (t, d, n)"},
-        "hbm": {"achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBPS, "bytes_per_launch": nbytes},
-        # decays exp(-dt A): one v_exp_f32 per (t, d, n); the peak is the
-        # quarter-rate transcendental issue of 1024 SIMDs at 2.4 GHz
-        "exp": {"achieved": B * L * D * N / (ev_ms * 1e-3), "peak": EXP_PEAK_PER_S,
-                "unit": "exp/s", "frac": B * L * D * N / (ev_ms * 1e-3) / EXP_PEAK_PER_S},
+                     "kernel_ms": ev_ms, "bytes_per_launch": nbytes,
+                     "bytes_rule": "x, dt, z, y 2 B per (t, d); B, C 2 B per (t, n); "
+                                   "hT 2 B per (d, n); A, Dskip once"},
+        # what actually bounds the kernel: its vector-ALU work
+        "alu": {"flops_per_tdn": FLOPS_PER_TDN, "exp_per_tdn": 1,
+                "achieved_tflops": FLOPS_PER_TDN * tdn / sec / 1e12,
+                "peak_tflops": VALU_PEAK_TFLOPS,
+                "frac": FLOPS_PER_TDN * tdn / sec / 1e12 / VALU_PEAK_TFLOPS,
+                "exp_per_s": tdn / sec, "exp_peak_per_s": EXP_PEAK_PER_S,
+                "exp_frac": tdn / sec / EXP_PEAK_PER_S,
+                "issue_slot_utilisation": {
+                    "slots_per_tdn": SLOTS_PER_TDN,
+                    "note": "exp = 4 slots (quarter rate), mul, mul, fma, fma = 1 each; "
+                            "peak 7.86e13 slots/s = 157.3 TFLOP/s / 2",
+                    "achieved_slots_per_s": SLOTS_PER_TDN * tdn / sec,
+                    "peak_slots_per_s": SLOT_PEAK_PER_S,
+                    "frac": SLOTS_PER_TDN * tdn / sec / SLOT_PEAK_PER_S}},
     }
+    cpu = None
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline_corpus(inp, wl, args.cpu_rows)
+        thr, nproc, aff = host_cpus()
+        # all 64 chunks with the thread share, eight chunks per call
+        t_all = sum(oracle_scan_time(inp, b0, b0 + 8, threads=thr) for b0 in range(0, B, 8))
+        # one thread on one chunk (3000 tokens, all channels)
+        t_one = oracle_scan_time(inp, 0, 1, threads=1)
+        cpu = {"value": tokens / t_all, "unit": "tokens/s", "cores": thr, "kind": "oracle",
+               "sample": "the whole workload (64 chunks x 3000 tokens x 2048 channels, N=16), "
+                         "fp64, %d threads, %.2f s" % (thr, t_all),
+               "nproc": nproc, "affinity_cpus": aff, "cpu": cpu_model(),
+               "single_thread": {"value": L / t_one, "unit": "tokens/s", "cores": 1,
+                                 "sample": "1 chunk x 3000 tokens x 2048 channels, %.2f s"
+                                           % t_one},
+               "gpu_over_oracle": (tokens / (ms * 1e-3)) / (tokens / t_all)}
     del inp, y, hT, ws
     torch.cuda.empty_cache()
-    return out
+    return out, cpu
 
 
-def bench_extra(args):
+# ----------------------------------------------------------------------------
+# the other workloads
+# ----------------------------------------------------------------------------
+def make_flush():
+    import torch
+
+    buf = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
+    return buf, (lambda: buf.zero_())  # evicts the 256 MB last-level cache
+
+
+def bench_single_layer(args, flush):
+    """One fp32 layer, B=1, L=512, D=128, N=16 (latency; the whole problem
+    fits in the last-level cache), and the same split at t = 384 with the
+    intermediate state passed in fp32 (Theorem 1)."""
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    wl = synth.SINGLE_LAYER
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = {k: v.cuda() for k, v in synth.scan_inputs_host(B, L, D, N, wl.seed,
+                                                           torch.float32).items()}
+    y = torch.empty((B, L, D), dtype=torch.float32, device="cuda")
+    hT = torch.empty((B, D, N), dtype=torch.float32, device="cuda")
+    h1 = torch.empty((B, D, N), dtype=torch.float32, device="cuda")
+    s = 384
+    # the automatic chunking (128 channels fill 2 waves, so time is cut into
+    # chunks: summary pass, carry fold, replay), and one pass over the sequence
+    desc = P.scan_desc(B, L, D, N, P.F32, P.F32, P.F32)
+    d1 = P.scan_desc(B, s, D, N, P.F32, P.F32, P.F32)
+    d2 = P.scan_desc(B, L - s, D, N, P.F32, P.F32, P.F32)
+    one = P.scan_desc(B, L, D, N, P.F32, P.F32, P.F32, chunk=L)
+    nws = max(P.scan_workspace_bytes(v) for v in (desc, d1, d2))
+    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    sl = lambda t, a, b: t[:, a:b]
+
+    def whole(dsc=desc):
+        P.scan_encode(dsc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], None, y, hT, ws, nws)
+
+    def split():
+        P.scan_encode(d1, sl(inp["x"], 0, s), sl(inp["dt"], 0, s), inp["A"], sl(inp["B"], 0, s),
+                      sl(inp["C"], 0, s), sl(inp["z"], 0, s), inp["Dskip"], None,
+                      sl(y, 0, s), h1, ws, nws)
+        P.scan_encode(d2, sl(inp["x"], s, L), sl(inp["dt"], s, L), inp["A"],
+                      sl(inp["B"], s, L), sl(inp["C"], s, L), sl(inp["z"], s, L), inp["Dskip"],
+                      h1, sl(y, s, L), hT, ws, nws)
+
+    nb = scan_bytes(B, L, D, N, in_bytes=4, y_bytes=4, st_bytes=4)
+    cold = time_events(whole, 20, flush, hold=True)
+    warm = time_events(whole, 50, None, hold=True)
+    res = {"workload": wl.name + ", y and hT fp32, h0 = 0",
+           "timing": "GPU time (stream held while the host enqueues); cold = after a 512 MB "
+                     "cache flush",
+           "workspace_bytes": nws,
+           "cold_us": cold * 1e3, "warm_us": warm * 1e3,
+           "one_pass_cold_us": time_events(lambda: whole(one), 20, flush, hold=True) * 1e3,
+           "one_pass_warm_us": time_events(lambda: whole(one), 50, None, hold=True) * 1e3,
+           "split_384_cold_us": time_events(split, 20, flush, hold=True) * 1e3,
+           "split_384_warm_us": time_events(split, 50, None, hold=True) * 1e3,
+           "tokens_per_s_warm": L / (warm * 1e-3)}
+    res.update(rates(nb, cold))
+    res["gbps_warm"] = nb / (warm * 1e-3) / 1e9
+    if not args.no_cpu:
+        thr = host_cpus()[0]
+        t1 = min(oracle_scan_time(inp, 0, 1, threads=1) for _ in range(3))
+        tn = min(oracle_scan_time(inp, 0, 1, threads=thr) for _ in range(3))
+        res["oracle"] = {"kind": "oracle", "sample": "the whole workload, fp64",
+                         "us_1_thread": t1 * 1e6, "us_threads": tn * 1e6, "threads": thr,
+                         "tokens_per_s_1_thread": L / t1}
+    return res
+
+
+def bench_query_path(args, flush):
+    """Query time (Sec. 4.2): top-1 retrieval of 256 queries over 10,000
+    unit-norm 384-dim keys, then the 32-token bf16 prefill starting from the
+    retrieved rows of a [10000, 1024, 16] fp16 state store (the injection
+    fused into the scan), cold cache."""
+    import numpy as np
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    cfg = synth.RETRIEVAL
+    Q, M, E = cfg["Q"], cfg["M"], cfg["E"]
+    q_h, K_h, _, _ = synth.retrieval_inputs_host(Q, M, E, cfg["planted"], cfg["seed"])
+    q, K = q_h.cuda(), K_h.cuda()
+    wl = synth.QUERY_PREFILL
+    D, N, Lq = wl.dim, wl.dstate, wl.seqlen
+    store = synth.state_store(M, D * N, seed=33, device="cuda")
+    store3 = store.view(M, D, N)
+    idx = torch.empty(Q, dtype=torch.int32, device="cuda")
+    nws = P.retrieve_workspace_bytes(Q, M, E)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    inp = synth.scan_inputs_device(Q, Lq, D, N, wl.seed, torch.bfloat16)
+    h0 = torch.empty((Q, D, N), dtype=torch.float16, device="cuda")
+    y = torch.empty((Q, Lq, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((Q, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(Q, Lq, D, N, P.BF16, P.BF16, P.F16)
+    prepared = P.prepare_index(K)
+
+    retrieve = lambda: P.retrieve_top1(q, K, idx, ws, nws)
+    prefill = lambda: P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"],
+                                            inp["C"], inp["z"], inp["Dskip"], store3, M, idx,
+                                            y, hT)
+
+    def fused():
+        retrieve()
+        prefill()
+
+    def fused_prepared():
+        P.retrieve_topk_prepared(q, K, prepared, 1, idx, None, ws, nws)
+        prefill()
+
+    def separate():
+        retrieve()
+        P.inject_gather(store, idx, h0.view(Q, -1))
+        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], h0, y, hT)
+
+    r_ms = time_events(retrieve, 20, flush, hold=True)
+    p_ms = time_events(prefill, 20, flush, hold=True)
+    f_ms = time_events(fused, 20, flush, hold=True)
+    fw_ms = time_events(fused, 20, None, hold=True)
+    fp_ms = time_events(fused_prepared, 20, flush, hold=True)
+    s_ms = time_events(separate, 20, flush, hold=True)
+    flops = 2.0 * Q * M * E
+    rbytes = (Q + M) * E * 4 + Q * 4
+    pbytes = scan_bytes(Q, Lq, D, N, h0_bytes=2)  # the injected rows are read once
+    res = {"workload": "Q=256 over M=10000 x 384 unit-norm fp32 keys; store [10000, 1024, 16] "
+                       "fp16; 32-token bf16 prefill from the retrieved rows, bf16 y, fp16 hT",
+           "timing": "GPU time (stream held while the host enqueues), after a 512 MB cache "
+                     "flush unless warm",
+           "end_to_end_fused_top1_us": f_ms * 1e3,
+           "end_to_end_fused_top1_warm_us": fw_ms * 1e3,
+           "end_to_end_fused_top1_prepared_index_us": fp_ms * 1e3,
+           "end_to_end_separate_gather_us": s_ms * 1e3,
+           "retrieve_top1_us": r_ms * 1e3,
+           "retrieve_bytes": rbytes, "retrieve_gbps": rbytes / (r_ms * 1e-3) / 1e9,
+           "retrieve_mfma_frac": flops / (r_ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS,
+           "prefill_indexed_us": p_ms * 1e3,
+           "queries_per_s": Q / (f_ms * 1e-3)}
+    res.update(rates(rbytes + pbytes, f_ms))
+    res["prefill_gbps"] = pbytes / (p_ms * 1e-3) / 1e9
+    res["prefill_hbm_frac"] = res["prefill_gbps"] / HBM_PEAK_GBPS
+    if not args.no_cpu:
+        import oracle
+
+        thr = host_cpus()[0]
+        store_h = store.cpu()
+        a = f64_rows(inp, 0, Q)
+        out = {"kind": "oracle", "sample": "the whole workload: fp64 brute-force top-1 over all "
+                                           "10,000 keys, gather, fp64 prefill", "threads": thr}
+        for name, t in (("1_thread", 1), ("threads", thr)):
+            t0 = time.perf_counter()
+            ridx, _ = oracle.top1(q_h, K_h, nthreads=t)
+            t1 = time.perf_counter()
+            h0o = oracle.gather(store_h, ridx).reshape(Q, D, N)
+            t2 = time.perf_counter()
+            oracle.scan(a["x"], a["dt"], a["A"], a["B"], a["C"], a["z"], a["Dskip"], h0o,
+                        nthreads=t)
+            t3 = time.perf_counter()
+            out["ms_" + name] = (t3 - t0) * 1e3
+            out["retrieve_ms_" + name] = (t1 - t0) * 1e3
+            out["prefill_ms_" + name] = (t3 - t2) * 1e3
+        res["oracle"] = out
+        del store_h, a
+    del inp, y, hT, h0, store, ws, q, K, prepared
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_long_context(args):
+    """8 x 65,536 tokens, D=2048, N=16, bf16, scanned in 256-token chunks
+    (summary pass, carry fold, replay)."""
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    wl = synth.LONG_CONTEXT
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
+    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((B, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=wl.chunk)
+    nws = P.scan_workspace_bytes(desc)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"],
+                                inp["z"], inp["Dskip"], None, y, hT, ws, nws)
+    ms = time_events(run, 5)
+    tdn = B * L * D * N
+    res = {"workload": wl.name + ", bf16 y, fp16 hT", "ms": ms,
+           "tokens_per_s": B * L / (ms * 1e-3), "workspace_bytes": nws,
+           "exp_per_s": 2 * tdn / (ms * 1e-3),
+           "exp_note": "two decays per (t, d, n): the summary pass and the replay"}
+    res.update(rates(scan_bytes(B, L, D, N), ms))
+    if not args.no_cpu:
+        thr = host_cpus()[0]
+        t_all = sum(oracle_scan_time(inp, b, b + 1, threads=thr) for b in range(B))
+        t_one = oracle_scan_time(inp, 0, 1, L=4096, threads=1)
+        res["oracle"] = {"kind": "oracle", "threads": thr,
+                         "sample": "the whole workload (8 x 65,536 tokens), fp64, one batch "
+                                   "row per call, %.1f s" % t_all,
+                         "tokens_per_s": B * L / t_all,
+                         "tokens_per_s_1_thread": 4096 / t_one,
+                         "sample_1_thread": "first 4096 tokens of row 0, all channels"}
+    del inp, y, hT, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_large_corpus(args):
+    """1024 chunks x 3000 tokens, D=1536, N=64, bf16, state-only (y NULL),
+    24 layers each with its own seeded inputs (seed 5000 + layer), every
+    layer's final states written into a [1024, 24, 1536, 64] fp16 store."""
+    import torch
+
+    from paper_2608_02560_amd import precog as P
+    from paper_2608_02560_amd import synth
+
+    wl = synth.LARGE_CORPUS
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    nl = synth.LARGE_CORPUS_LAYERS
+    store = torch.empty((B, nl, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.F32, P.F16, hT_batch_stride=nl * D * N)
+    per_layer = []
+    cpu_inp = None
+    for layer in range(nl):
+        inp = synth.scan_inputs_device(B, L, D, N, wl.seed + layer, torch.bfloat16, wl.dt_mu,
+                                       wl.dt_sigma, need_z_c=False)
+        run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
+                                    None, None, None, store[:, layer])
+        per_layer.append(time_events(run, 1))
+        if layer == 0 and not args.no_cpu:
+            cpu_inp = {k: (v[:16].clone() if v is not None and v.dim() == 3 else v)
+                       for k, v in inp.items()}
+        del inp
+    torch.cuda.synchronize()
+    total = sum(per_layer)
+    tdn = B * L * D * N
+    nb = scan_bytes(B, L, D, N, readout=False)
+    mean = total / nl
+    res = {"workload": wl.name + ", state-only, fp16 states into the 24-layer store",
+           "layers": nl, "ms_24_layers": total, "ms_per_layer_mean": mean,
+           "ms_per_layer_min": min(per_layer), "ms_per_layer_max": max(per_layer),
+           "timing": "each layer's inputs drawn on the device (untimed), one untimed call, "
+                     "then one event-timed call; the 24 timed calls summed",
+           "chunk_tokens_per_s_24_layers": B * L / (total * 1e-3),
+           "tokens_per_s_per_layer": B * L / (mean * 1e-3),
+           "exp_per_s": tdn / (mean * 1e-3), "exp_frac": tdn / (mean * 1e-3) / EXP_PEAK_PER_S}
+    res.update(rates(nb, mean))
+    if cpu_inp is not None:
+        thr = host_cpus()[0]
+        t16 = oracle_scan_time(cpu_inp, 0, 16, threads=thr, want_y=False)
+        t1 = oracle_scan_time(cpu_inp, 0, 1, threads=1, want_y=False)
+        res["oracle"] = {"kind": "oracle", "threads": thr,
+                         "sample": "layer 0, 16 of 1024 chunks, state-only, fp64, %.2f s; "
+                                   "extrapolated linearly to 1024 chunks x 24 layers" % t16,
+                         "tokens_per_s_per_layer": 16 * L / t16,
+                         "chunk_tokens_per_s_24_layers_extrapolated": 16 * L / t16 / nl,
+                         "ms_24_layers_extrapolated": t16 * (B / 16) * nl * 1e3,
+                         "tokens_per_s_per_layer_1_thread": L / t1,
+                         "sample_1_thread": "layer 0, 1 chunk"}
+    del store, cpu_inp
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_extensions(args, flush):
+    """Top-k retrieval + softmax composition, the SMC trajectory at three
+    dials, SMC routing / consolidation / session start, and the complex-A
+    scan on the corpus-encode shape."""
     import torch
 
     from paper_2608_02560_amd import precog as P
     from paper_2608_02560_amd import synth
 
     res = {}
-    flush_buf = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
-    flush = lambda: flush_buf.zero_()  # evicts the 256 MB last-level cache
-
-    # query-time path
     cfg = synth.RETRIEVAL
-    q, K, _, _ = synth.retrieval_inputs_host(cfg["Q"], cfg["M"], cfg["E"], cfg["planted"],
-                                             cfg["seed"])
+    Q, M, E = cfg["Q"], cfg["M"], cfg["E"]
+    q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, cfg["planted"], cfg["seed"])
     q, K = q.cuda(), K.cuda()
     wl = synth.QUERY_PREFILL
-    D, N = wl.dim, wl.dstate
-    store = synth.state_store(cfg["M"], D * N, seed=33, device="cuda")
-    idx = torch.empty(cfg["Q"], dtype=torch.int32, device="cuda")
-    nws = P.retrieve_workspace_bytes(cfg["Q"], cfg["M"], cfg["E"])
+    D, N, Lq = wl.dim, wl.dstate, wl.seqlen
+    store = synth.state_store(M, D * N, seed=33, device="cuda")
+    store3 = store.view(M, D, N)
+    nws = P.retrieve_workspace_bytes(Q, M, E)
     ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
-    inp = synth.scan_inputs_device(wl.batch, wl.seqlen, D, N, wl.seed, torch.bfloat16)
-    h0 = torch.empty((wl.batch, D, N), dtype=torch.float16, device="cuda")
-    y = torch.empty((wl.batch, wl.seqlen, D), dtype=torch.bfloat16, device="cuda")
-    hT = torch.empty((wl.batch, D, N), dtype=torch.float16, device="cuda")
-    desc = P.scan_desc(wl.batch, wl.seqlen, D, N, P.BF16, P.BF16, P.F16)
-    r_ms = time_events(lambda: P.retrieve_top1(q, K, idx, ws, nws), 20, flush, hold=True)
-    g_ms = time_events(lambda: P.inject_gather(store, idx, h0.view(wl.batch, -1)), 20, flush,
-                       hold=True)
-    s_ms = time_events(lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"],
-                                             inp["C"], inp["z"], inp["Dskip"], h0, y, hT), 20,
-                       flush, hold=True)
-
-    def pipeline():
-        P.retrieve_top1(q, K, idx, ws, nws)
-        P.inject_gather(store, idx, h0.view(wl.batch, -1))
-        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
-                      inp["Dskip"], h0, y, hT)
-
-    e_ms = time_events(pipeline, 20, flush, hold=True)
-
-    # the same path with the injection fused into the prefill
-    # (precog_scan_encode_indexed reads store[idx] rows directly)
-    store3 = store.view(cfg["M"], D, N)
-    f_ms = time_events(lambda: P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"],
-                                                     inp["C"], inp["z"], inp["Dskip"], store3,
-                                                     cfg["M"], idx, y, hT), 20, flush, hold=True)
-
-    def pipeline_fused():
-        P.retrieve_top1(q, K, idx, ws, nws)
-        P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
-                              inp["Dskip"], store3, cfg["M"], idx, y, hT)
-
-    ef_ms = time_events(pipeline_fused, 20, flush, hold=True)
-    eh_ms = time_events(pipeline_fused, 20, flush)
-    # the same path with the inputs left in the caches by the previous call
-    # (as when the query tokens come straight from the layer before)
-    ew_ms = time_events(pipeline_fused, 20, None, hold=True)
-    # the same path recorded once in a HIP graph and replayed (cold cache)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        pipeline_fused()
-    torch.cuda.synchronize()
-    eg_ms = time_events(graph.replay, 20, flush, hold=True)
-    del graph
-    # retrieval over the index prepared once (screen operands and norms made
-    # offline, as the keys are), alone and in the fused top-1 path
-    prepared = P.prepare_index(K)
-    pbytes = prepared.numel()
-    rp_ms = time_events(lambda: P.retrieve_topk_prepared(q, K, prepared, 1, idx, None, ws, nws), 20,
-                        flush, hold=True)
-
-    def pipeline_fused_prepared():
-        P.retrieve_topk_prepared(q, K, prepared, 1, idx, None, ws, nws)
-        P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
-                              inp["Dskip"], store3, cfg["M"], idx, y, hT)
-
-    efp_ms = time_events(pipeline_fused_prepared, 20, flush, hold=True)
-    flops = 2.0 * cfg["Q"] * cfg["M"] * cfg["E"]
-    sbytes = scan_bytes(wl.batch, wl.seqlen, D, N) + wl.batch * D * N * 2
-    res["query_path"] = {
-        "workload": "Q=256 over M=10000 x 384 keys; store [10000, 1024, 16] fp16; "
-                    "32-token bf16 query prefill; cold last-level cache",
-        "timing": "GPU time: the stream is held by a bounded spin while the host enqueues "
-                  "each timed call; end_to_end_fused_host_ms includes host launch latency; "
-                  "end_to_end_fused_warm_ms runs without the cache flush; "
-                  "end_to_end_fused_graph_ms replays the path recorded in a HIP graph; "
-                  "*_prepared_ms use the index prepared once (precog_retrieve_prepare)",
-        "retrieve_ms": r_ms, "retrieve_tflops": flops / (r_ms * 1e-3) / 1e12,
-        # the screen's contraction runs as fp16 MFMA (one product per feature):
-        # the fraction is taken against the dense fp16 peak
-        "retrieve_mfma_frac": flops / (r_ms * 1e-3) / 2500e12,
-        "gather_ms": g_ms, "gather_gbps": 2 * wl.batch * D * N * 2 / (g_ms * 1e-3) / 1e9,
-        "prefill_ms": s_ms, "prefill_gbps": sbytes / (s_ms * 1e-3) / 1e9,
-        "end_to_end_ms": e_ms,
-        "fused_inject_prefill_ms": f_ms,
-        "end_to_end_fused_ms": ef_ms,
-        "end_to_end_fused_host_ms": eh_ms,
-        "end_to_end_fused_warm_ms": ew_ms,
-        "end_to_end_fused_graph_ms": eg_ms,
-        "retrieve_prepared_ms": rp_ms,
-        "end_to_end_fused_prepared_ms": efp_ms,
-        "prepared_index_bytes": pbytes,
-    }
-
-    # top-k variant: top-3 retrieval with scores, softmax composition into h0
+    inp = synth.scan_inputs_device(Q, Lq, D, N, wl.seed, torch.bfloat16)
+    y = torch.empty((Q, Lq, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((Q, D, N), dtype=torch.float16, device="cuda")
+    h0 = torch.empty((Q, D, N), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(Q, Lq, D, N, P.BF16, P.BF16, P.F16)
     kk = 3
-    idxk = torch.empty((cfg["Q"], kk), dtype=torch.int32, device="cuda")
-    sck = torch.empty((cfg["Q"], kk), dtype=torch.float64, device="cuda")
+    idxk = torch.empty((Q, kk), dtype=torch.int32, device="cuda")
+    sck = torch.empty((Q, kk), dtype=torch.float64, device="cuda")
     rk_ms = time_events(lambda: P.retrieve_topk(q, K, kk, idxk, sck, ws, nws), 20, flush,
                         hold=True)
-    P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
-    c_ms = time_events(lambda: P.inject_compose(store, idxk, sck, 1.0, h0.view(wl.batch, -1)), 20,
+    c_ms = time_events(lambda: P.inject_compose(store, idxk, sck, 1.0, h0.view(Q, -1)), 20,
                        flush, hold=True)
 
-    def pipeline_k():
-        P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
-        P.inject_compose(store, idxk, sck, 1.0, h0.view(wl.batch, -1))
-        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
-                      inp["Dskip"], h0, y, hT)
-
-    ek_ms = time_events(pipeline_k, 20, flush, hold=True)
-
-    # the top-3 path with the composition fused into the prefill
-    def pipeline_k_fused():
+    def fused_k():
         P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
         P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
-                              inp["Dskip"], store3, cfg["M"], idxk, y, hT, h0_score=sck, k=kk,
-                              tau=1.0)
+                              inp["Dskip"], store3, M, idxk, y, hT, h0_score=sck, k=kk, tau=1.0)
 
-    ekf_ms = time_events(pipeline_k_fused, 20, flush, hold=True)
-    res["query_path_topk"] = {
-        "workload": "as query_path with top-3 retrieval and softmax composition (tau = 1)",
-        "retrieve_topk_ms": rk_ms,
-        "compose_ms": c_ms,
-        "compose_gbps": (kk + 1) * wl.batch * D * N * 2 / (c_ms * 1e-3) / 1e9,
-        "end_to_end_ms": ek_ms,
-        "end_to_end_fused_ms": ekf_ms,
-    }
-    del inp, y, hT, h0, store, ws, q, K, prepared
+    res["query_path_top3"] = {
+        "workload": "the query path with top-3 retrieval and softmax composition (tau = 1), "
+                    "cold cache, GPU time",
+        "retrieve_top3_us": rk_ms * 1e3, "compose_us": c_ms * 1e3,
+        "compose_gbps": (kk + 1) * Q * D * N * 2 / (c_ms * 1e-3) / 1e9,
+        "end_to_end_fused_us": time_events(fused_k, 20, flush, hold=True) * 1e3}
+    del inp, y, hT, h0, store, ws, q, K
     torch.cuda.empty_cache()
 
-    # SMC trajectory encode at the fidelity dials (state-only, fp16 states)
     wl = synth.SMC_TRAJECTORY
     B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
     inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, need_z_c=False)
     desc = P.scan_desc(B, L, D, N, P.BF16, P.F32, P.F16)
-    nws = P.scan_workspace_bytes(desc)
-    ws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
     traj_res = {"workload": wl.name + ", state-only, fp16 states"}
     for every in synth.SMC_DIALS:
         traj = torch.empty((B, L // every, D, N), dtype=torch.float16, device="cuda")
         run = lambda: P.scan_trajectory(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
-                                        None, None, None, None, traj, every, ws, nws)
+                                        None, None, None, None, traj, every)
         t_ms = time_events(run, 5)
         nb = scan_bytes(B, L, D, N, readout=False) - B * D * N * 2 + traj.numel() * 2
         traj_res["every_%d" % every] = {"ms": t_ms, "tokens_per_s": B * L / (t_ms * 1e-3),
-                                        "gbps": nb / (t_ms * 1e-3) / 1e9,
-                                        "states_kept_per_chunk": L // every}
+                                        "states_kept_per_chunk": L // every, **rates(nb, t_ms)}
         del traj
     res["smc_trajectory"] = traj_res
-    del inp, ws
+    del inp
     torch.cuda.empty_cache()
 
-    # SMC consolidation: route 64 chunks, fold their final states into the
-    # 20 semantic states (24 x 4096, fp16), then a session start (route the
-    # opening chunk, inject its semantic state)
     cfg = synth.SMC
     emb, dom, sub, _, _ = synth.smc_inputs_host(cfg["C"], cfg["E"], cfg["ndom"], cfg["nsub"],
                                                 cfg["seed"])
@@ -406,19 +637,15 @@ def bench_extra(args):
         P.smc_route(emb[:1], dom, sub, *one)
         P.inject_gather(states, one[2], h_init)
 
-    se_ms = time_events(session, 20, hold=True)
     res["smc"] = {
         "workload": "64 chunks routed over 5 domains x 4 sub-clusters (E=384); semantic states "
-                    "[20, 24 x 4096] fp16, alpha = 0.2",
-        "timing": "GPU time: the stream is held by a bounded spin while the host enqueues",
-        "route_ms": ro_ms, "consolidate_ms": co_ms,
+                    "[20, 24 x 4096] fp16, alpha = 0.2; GPU time",
+        "route_us": ro_ms * 1e3, "consolidate_us": co_ms * 1e3,
         "consolidate_gbps": (2 * R * S * 2 + cfg["C"] * S * 2) / (co_ms * 1e-3) / 1e9,
-        "session_start_ms": se_ms,
-    }
+        "session_start_us": time_events(session, 20, hold=True) * 1e3}
     del states, contrib
     torch.cuda.empty_cache()
 
-    # complex-A scan on the corpus-encode shape (w_n = pi n)
     wl = synth.COMPLEX_ENCODE
     B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
     inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
@@ -428,54 +655,13 @@ def bench_extra(args):
     desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16)
     run = lambda: P.scan_complex_raw(desc, inp["x"], inp["dt"], inp["A"], A_im, inp["B"],
                                      inp["C"], inp["z"], inp["Dskip"], None, y, hT)
-    run()
     x_ms = time_events(run, 5)
-    nb = scan_bytes(B, L, D, N) + B * D * N * 2  # hT has two parts
     res["complex_encode"] = {"workload": wl.name + ", w_n = pi n, fp16 complex hT",
                              "ms": x_ms, "tokens_per_s": B * L / (x_ms * 1e-3),
-                             "gbps": nb / (x_ms * 1e-3) / 1e9,
-                             "transcendentals_per_s": 3 * B * L * D * N / (x_ms * 1e-3)}
+                             "transcendentals_per_s": 3 * B * L * D * N / (x_ms * 1e-3),
+                             **rates(scan_bytes(B, L, D, N) + B * D * N * 2, x_ms)}
     del inp, y, hT, A_im
     torch.cuda.empty_cache()
-
-    # long-context chunked scan (one timed call)
-    wl = synth.LONG_CONTEXT
-    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
-    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
-    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
-    hT = torch.empty((B, D, N), dtype=torch.float16, device="cuda")
-    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=wl.chunk)
-    nws = P.scan_workspace_bytes(desc)
-    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
-    run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"],
-                                inp["z"], inp["Dskip"], None, y, hT, ws, nws)
-    run()
-    l_ms = time_events(run, 5)
-    nb = scan_bytes(B, L, D, N)
-    res["long_context"] = {"workload": wl.name, "ms": l_ms, "tokens_per_s": B * L / (l_ms * 1e-3),
-                           "gbps": nb / (l_ms * 1e-3) / 1e9}
-    del inp, y, hT, ws
-    torch.cuda.empty_cache()
-
-    # one layer of the large corpus encode (state-only)
-    wl = synth.LARGE_CORPUS
-    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
-    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16, wl.dt_mu, wl.dt_sigma,
-                                   need_z_c=False)
-    store = torch.empty((B, 24, D, N), dtype=torch.float16, device="cuda")
-    desc = P.scan_desc(B, L, D, N, P.BF16, P.F32, P.F16, hT_batch_stride=24 * D * N)
-    run = lambda: P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
-                                None, None, None, store[:, 0])
-    run()
-    c_ms = time_events(run, 3)
-    nb = scan_bytes(B, L, D, N, readout=False)
-    res["large_corpus_layer"] = {"workload": wl.name, "ms": c_ms,
-                                 "tokens_per_s": B * L / (c_ms * 1e-3),
-                                 "gbps": nb / (c_ms * 1e-3) / 1e9,
-                                 "exp_per_s": B * L * D * N / (c_ms * 1e-3),
-                                 "exp_frac": B * L * D * N / (c_ms * 1e-3) / EXP_PEAK_PER_S,
-                                 # all 24 layers of a chunk batch, one layer per launch
-                                 "chunk_tokens_per_s_24_layers": B * L / (24 * c_ms * 1e-3)}
     return res
 
 
@@ -484,10 +670,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--chunk", type=int, default=0)
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=32)
-    ap.add_argument("--extra", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true", help="skip every oracle timing")
+    ap.add_argument("--quick", action="store_true", help="time the headline workload only")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (traffic-counter calibration)")
     args = ap.parse_args()
@@ -509,9 +693,25 @@ def main():
         print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n,
                           "launches": 3}), flush=True)
         return
-    out = bench_corpus(args)
-    if args.extra:
-        out["extra"] = bench_extra(args)
+    t_start = time.perf_counter()
+    out, cpu = bench_corpus(args)
+    log("corpus encode done (%.1f s)" % (time.perf_counter() - t_start))
+    if not args.quick:
+        buf, flush = make_flush()
+        cfgs = {}
+        for name, fn in (("single_layer", lambda: bench_single_layer(args, flush)),
+                         ("query_path", lambda: bench_query_path(args, flush)),
+                         ("long_context", lambda: bench_long_context(args)),
+                         ("large_corpus", lambda: bench_large_corpus(args))):
+            cfgs[name] = fn()
+            log("%s done (%.1f s)" % (name, time.perf_counter() - t_start))
+        out["configs"] = cfgs
+        out["extensions"] = bench_extensions(args, flush)
+        log("extensions done (%.1f s)" % (time.perf_counter() - t_start))
+        del buf
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    out["bench_wall_s"] = time.perf_counter() - t_start
     print(json.dumps(out), flush=True)
 
 
