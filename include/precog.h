@@ -242,7 +242,9 @@ size_t precog_retrieve_workspace_bytes(int64_t Q, int64_t M, int64_t E);
  *   idx        [Q] int32 output; M == 0 gives -1
  *   E % 4 == 0, 4 <= E <= 4096; pointers 16-byte aligned.
  *   workspace  precog_retrieve_workspace_bytes(Q, M, E) bytes, 16-byte
- *              aligned, about 4 Q M + 4 M bytes (the screen scores);
+ *              aligned, about 9 Q M / 32 + 4 M bytes (per query and
+ *              32-key block the screen keeps its largest score, that key
+ *              and the second largest);
  *              ceil(M / 32) * ceil(Q / 128) must not exceed 2^31 - 1. */
 precog_status precog_retrieve_top1(const float *query_emb,
                                    const float *index_emb, int64_t Q, int64_t M,
@@ -275,7 +277,7 @@ precog_status precog_retrieve_top1(const float *query_emb,
  * nothing (no hipMalloc, hipFree or allocating library routine); its first
  * call on a device looks up that device's copy of the array.
  *   Limit: precog_retrieve_workspace_bytes(Q, M, E) must not exceed
- *   PRECOG_NOALLOC_SCRATCH_BYTES (about Q * M <= 8.3e6 pairs), else
+ *   PRECOG_NOALLOC_SCRATCH_BYTES (about Q * M <= 1.1e8 pairs), else
  *   PRECOG_ERR_WORKSPACE and nothing is enqueued.
  *   Every call on one device shares that device's array: calls that overlap
  *   on one device (different streams without ordering between them, or

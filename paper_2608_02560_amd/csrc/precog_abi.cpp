@@ -289,23 +289,26 @@ precog_status precog_scan_trajectory(const precog_scan_desc* desc, const void* x
 }
 
 namespace {
-// Retrieval workspace: query operands ([nqg, nks, 64] x 16 B), screen
-// scores [Q, 32 nkb], block maxima [Q, nkb], key norms [M] and block norms
-// [nkb], each 256-byte aligned.
+// Retrieval workspace: query operands ([nqg, nks, 64] x 16 B), the screen's
+// per-(query, 32-key block) summaries -- largest score [Q, nkb], second
+// largest [Q, nkb], key of the largest [Q, nkb] (1 B) -- key norms [M] and
+// block norms [nkb], each 256-byte aligned: about 9 Q M / 32 bytes.
 struct RetrieveWs {
-  size_t qop, scores, blockmax, rownorm, blocknorm, total;
+  size_t qop, blockmax, blocksec, blockarg, rownorm, blocknorm, total;
 };
 RetrieveWs retrieve_ws(int64_t Q, int64_t M, int64_t E) {
   RetrieveWs w;
   const size_t nkb = static_cast<size_t>((M + 31) / 32);
-  const size_t nqg = static_cast<size_t>((Q + 127) / 128) * 4;
+  const size_t qpw = 32 * precog::kRetWaves;  // queries per screen workgroup
+  const size_t nqg = static_cast<size_t>((Q + qpw - 1) / qpw) * precog::kRetWaves;
   const size_t nks = static_cast<size_t>((E + 15) / 16);
   w.qop = align_up(nqg * nks * 64 * 16);
-  w.scores = align_up(static_cast<size_t>(Q) * nkb * 32 * 4);
   w.blockmax = align_up(static_cast<size_t>(Q) * nkb * 4);
+  w.blocksec = align_up(static_cast<size_t>(Q) * nkb * 4);
+  w.blockarg = align_up(static_cast<size_t>(Q) * nkb);
   w.rownorm = align_up(static_cast<size_t>(M) * 4);
   w.blocknorm = align_up(nkb * 4);
-  w.total = w.qop + w.scores + w.blockmax + w.rownorm + w.blocknorm;
+  w.total = w.qop + w.blockmax + w.blocksec + w.blockarg + w.rownorm + w.blocknorm;
   return w;
 }
 }  // namespace
@@ -377,7 +380,8 @@ precog_status retrieve_entry(const float* query_emb, const float* index_emb, con
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
-  // one screen workgroup per (32 keys, 128 queries): the grid must fit an int
+  // screen workgroups (at most one per 32 keys and 128 queries) and the
+  // workspace sizes must stay within their integer types
   if (ceil_div(M, 32) * ceil_div(Q, 128) > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   if (Q == 0) return PRECOG_OK;
   if (!query_emb || !idx) return PRECOG_ERR_NULL;
@@ -398,10 +402,12 @@ precog_status retrieve_entry(const float* query_emb, const float* index_emb, con
   if (M > 0) {
     p.qop = ws;
     char* at = ws + w.qop;
-    p.scores = reinterpret_cast<float*>(at);
-    at += w.scores;
     p.blockmax = reinterpret_cast<float*>(at);
     at += w.blockmax;
+    p.blocksec = reinterpret_cast<float*>(at);
+    at += w.blocksec;
+    p.blockarg = reinterpret_cast<uint8_t*>(at);
+    at += w.blockarg;
     p.rownorm2 = reinterpret_cast<float*>(at);
     at += w.rownorm;
     p.blocknorm2 = reinterpret_cast<float*>(at);
@@ -420,8 +426,8 @@ precog_status retrieve_entry(const float* query_emb, const float* index_emb, con
   p.M = M;
   p.E = E;
   p.nkb = static_cast<int>((M + 31) / 32);
-  p.ld_scores = static_cast<int64_t>(p.nkb) * 32;
-  p.nqg = static_cast<int>((Q + 127) / 128 * 4);
+  p.nqg = static_cast<int>((Q + 32 * precog::kRetWaves - 1) / (32 * precog::kRetWaves) *
+                           precog::kRetWaves);
   p.nks = static_cast<int>((E + 15) / 16);
   p.k = static_cast<int>(k);
   (void)hipGetLastError();

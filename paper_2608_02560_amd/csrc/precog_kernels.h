@@ -71,19 +71,23 @@ struct RetrieveParams {
   const float* K;      // [M, E]
   void* qop;           // fp16(2^8 q) in operand order (workspace)
   const void* kop;     // prepared index operands, or null (keys read as fp32)
-  float* scores;       // [Q, ld_scores] screen scores (workspace)
-  float* blockmax;     // [Q, nkb] max screen score per 32-key block (workspace)
+  float* blockmax;     // [Q, nkb] largest screen score per 32-key block (workspace)
+  float* blocksec;     // [Q, nkb] largest screen score of the block's other keys (workspace)
+  uint8_t* blockarg;   // [Q, nkb] key of the largest, 0..31 within its block (workspace)
   float* rownorm2;     // [M] squared key norms (workspace)
   float* blocknorm2;   // [nkb] largest squared key norm per block (workspace)
   int32_t* idx;        // [Q, k]
   double* score;       // [Q, k] exact scores of idx, or null
   int64_t Q, M, E;
-  int64_t ld_scores;   // row pitch of scores (M rounded up to 32)
   int nkb;             // ceil(M / 32)
-  int nqg;             // ceil(Q / 128) * 4: 32-query groups, padded to whole workgroups
+  int nqg;             // 32-query groups, padded to whole screen workgroups
   int nks;             // ceil(E / 16): 16-feature steps
   int k;               // keys kept per query, 1..kMaxTopK
 };
+// Screen workgroup: kRetWaves waves of 32 queries each, over kRetBlocks
+// blocks of 32 keys.
+constexpr int kRetWaves = 8;
+constexpr int kRetBlocks = 2;
 constexpr int kMaxTopK = 64;
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
 // Body of the retrieval entry points (precog_abi.cpp): validates the

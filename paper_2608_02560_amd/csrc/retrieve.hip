@@ -9,13 +9,14 @@
 //            components clear of the fp16 subnormal range) and stores the
 //            values in the order the matrix-core operands are consumed, so a
 //            wave's operand load is one contiguous 1 KiB segment.
-//   screen   workgroup = 32 keys x 128 queries: the keys are read
+//   screen   workgroup = 64 keys x 128 queries: the keys are read
 //            row-contiguously, rounded the same way and staged in LDS; each
-//            wave computes a 32 x 32 tile with v_mfma_f32_32x32x16_f16 (each
-//            product of two fp16 values is exact in fp32) and scales it back
-//            by 2^-16.  It stores every screen score S~_i, the maximum of each
-//            (query, 32-key block), and the squared norm of every key and the
-//            largest one of every block.
+//            wave computes 32 queries against them with
+//            v_mfma_f32_32x32x16_f16 (each product of two fp16 values is
+//            exact in fp32) and scales back by 2^-16.  For every (query,
+//            32-key block) it keeps the largest screen score S~, its key, and
+//            the largest S~ of the block's other keys; and the squared norm
+//            of every key and the largest one of every block.
 //   decide   one wave per query: m = the largest screen score.  A key can
 //            still be the fp64 maximum only if S~_i + e(i) >= m - e(i0), where
 //            e(i) = g |q| |k_i| + h (|q| + |k_i|) + tiny bounds the error of
@@ -25,12 +26,13 @@
 //            h bounds values below the fp16 normal range per unit of the
 //            1-norms; both are inflated for the fp32 norms and the fp64
 //            rounding of the reference).  Blocks are tested first with their
-//            maxima and norm bounds, then the keys of surviving blocks; every
-//            candidate is scored exactly in fp64 in index order and the best
-//            (score, lowest index) wins, so the result is exact.  A query or
-//            key of norm 245 or more could leave the fp16 range (2^8 |v| past
-//            65504); then the screen proves nothing and every key is scored
-//            in fp64.
+//            maxima and norm bounds; of a surviving block only its largest
+//            key is a candidate unless its second largest passes too, then
+//            every key of the block is; every candidate is scored exactly in
+//            fp64 in index order and the best (score, lowest index) wins, so
+//            the result is exact.  A query or key of norm 245 or more could
+//            leave the fp16 range (2^8 |v| past 65504); then the screen
+//            proves nothing and every key is scored in fp64.
 #include "precog_kernels.h"
 #include "wave_ops.h"
 
@@ -46,13 +48,12 @@ typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
 constexpr float kScale = 256.f;
 constexpr float kUnscale = 1.f / 65536.f;
 
-constexpr int kKB = 32;       // keys per block (screen workgroup, block maxima)
-constexpr int kQW = 32;       // queries per wave (one 32 x 32 tile)
-constexpr int kQWG = 4 * kQW; // queries per workgroup
+constexpr int kKB = 32;       // keys per block (one MFMA tile's rows; block summaries)
 // features per chunk: the wave preloads its query operands for a whole chunk
 // (kFC / 16 x 4 VGPRs)
 constexpr int kFC = 128;
 constexpr int kKS = kFC / 16; // 16-feature MFMA steps per chunk
+constexpr int kRound = 1;     // chunks whose loads the screen issues together
 
 __device__ __forceinline__ float xor_shfl(float v, int m) {
   const int src = (static_cast<int>(threadIdx.x & 63) ^ m) * 4;
@@ -88,24 +89,38 @@ __global__ __launch_bounds__(256) void prep_kernel(const RetrieveParams p) {
   reinterpret_cast<halfx8*>(p.qop)[t] = o8;
 }
 
-// screen: workgroup (kb, qg) = key block kb (keys 32 kb + 0..31) x queries
-// [128 qg, 128 qg + 128), wave w taking 32 of them.  Per feature chunk the
-// workgroup loads the block's key rows row-contiguously and every wave its
-// query operands, all before the first wait (one memory latency per chunk);
-// the keys are rounded and stored in LDS in operand order
-// [ks][h][row], the row index XOR-swizzled with (2 ks + h) so both the
-// staging writes and the operand reads hit distinct banks.  MFMA operands:
-// lane l supplies row / column l mod 32 and the 8 features of half
-// h = l / 32 of the 16-feature step, for queries and keys alike, so each dot
-// product is unchanged whatever order the instruction consumes features in.
-// Output register r holds query row 8 (r / 4) + 4 h + (r mod 4), key column
-// l mod 32; screen scores are stored as 128-byte runs of 32 keys.
+// screen: workgroup (kg, qg) = key blocks [kRetBlocks kg, kRetBlocks kg +
+// kRetBlocks) (32 keys each) x query groups [kRetWaves qg, kRetWaves qg +
+// kRetWaves) (32 queries each), wave w taking query group kRetWaves qg + w.
+// Per 128-feature chunk the workgroup stages its blocks' key rows in LDS,
+// rounded to fp16(2^8 k) and laid out in operand order [kb][ks][h][row],
+// the row XOR-swizzled with (2 ks + h) so the staging writes and the operand
+// reads hit distinct banks; every wave loads its own query operands; all of
+// a chunk's loads are issued before the first wait.  MFMA operands: keys are
+// the rows (A), queries the columns (B); lane l supplies row / column
+// l mod 32 and the 8 features of half h = l / 32 of the 16-feature step, so
+// each dot product is the same whatever order the instruction consumes
+// features in.  Output register r of lane l holds key row 8 (r / 4) + 4 h +
+// (r mod 4) and query column l mod 32, so the 32 keys of a block for one
+// query sit in the 16 registers of lanes l and l xor 32: the block's largest
+// screen score, its key and the largest of the other keys are found in
+// registers and one exchange between the two halves.  Per (query, block) the
+// screen stores those three (block maxima, second maxima, keys), not the
+// scores themselves.
 template <bool PREP>
-__global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
-  const int nqwg = static_cast<int>((p.Q + kQWG - 1) / kQWG);
+__global__ __launch_bounds__(64 * kRetWaves) void screen_kernel(const RetrieveParams p) {
+  constexpr int kT = 64 * kRetWaves;        // threads
+  constexpr int kRows = kKB * kRetBlocks;   // key rows per workgroup
+  constexpr int kC4 = kFC / 4;              // float4 columns per row and chunk
+  constexpr int kStage = kRows * kC4 / kT;  // float4 staged per thread and chunk
+  constexpr int kPK = kRetBlocks * kKS * 64 / kT;  // prepared entries per thread and chunk
+  static_assert(kRows * kC4 % kT == 0 && kRetBlocks * kKS * 64 % kT == 0,
+                "staging must divide evenly");
+  static_assert(kT % kC4 == 0, "a thread stages one column of several rows");
+  const int nqwg = static_cast<int>((p.Q + 32 * kRetWaves - 1) / (32 * kRetWaves));
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
-  const int kb = lb / nqwg;
-  const int qg = lb - kb * nqwg;
+  const int kg = lb / nqwg;
+  const int qg = lb - kg * nqwg;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave-uniform, so the operand descriptors below live in scalar registers
@@ -113,150 +128,184 @@ __global__ __launch_bounds__(256) void screen_kernel(const RetrieveParams p) {
   const int r32 = lane & 31;
   const int half = lane >> 5;
   const int64_t E = p.E;
-  const int64_t k0 = static_cast<int64_t>(kb) * kKB;
-  const int64_t qw = static_cast<int64_t>(qg) * kQWG + wave * kQW;  // first query of the wave
+  const int64_t k0 = static_cast<int64_t>(kg) * kRows;  // first key of the workgroup
+  const int64_t qw = (static_cast<int64_t>(qg) * kRetWaves + wave) * 32;  // first query of the wave
   const bool active = qw < p.Q;
   // its 32-query group in the split layout (clamped for waves past Q, whose
   // loads stay in bounds and whose results are discarded)
   const int64_t g = active ? qw / 32 : p.nqg - 1;
 
-  // double-buffered: chunk c is staged in buffer c mod 2, so one barrier per
-  // chunk separates the staging of c from the reads of c - 1 and c - 2
-  __shared__ halfx8 kop[2][kKS][2][32];
-  __shared__ float nsum[2][kKB];
+  // A round covers kRound chunks of kFC features: every load of the round
+  // is issued before the first wait, so a workgroup pays one memory latency
+  // per round (one for E <= kRound kFC), each chunk staged in its own LDS
+  // tile; one barrier then separates the staging from the reads, and a
+  // second one the reads from the next round's staging.
+  __shared__ halfx8 kop[kRound][kRetBlocks][kKS][2][32];
+  __shared__ float nsum[kRows];
 
-  const int srow_base = (tid >> 2) & 31;  // key row this thread stages
-  // the block's rows through a descriptor: rows past M read as zero
-  const int64_t nrows = p.M - k0 < kKB ? p.M - k0 : kKB;
+  // thread t stages float4 column t mod kC4 of rows t / kC4 + (kT / kC4) j
+  const int c4 = tid % kC4;
+  const int srow0 = tid / kC4;
+  const int64_t nrows = p.M - k0 < kRows ? p.M - k0 : kRows;  // rows past M read as zero
   const __amdgpu_buffer_rsrc_t kres =
       make_rsrc(p.K + k0 * E, static_cast<uint32_t>(nrows * E * 4));
-  const uint32_t krow_off = static_cast<uint32_t>(srow_base * E * 4);
-  float n2 = 0.f;                         // its share of that row's squared norm
+  float n2[kStage];  // this thread's share of its rows' squared norms
+#pragma unroll
+  for (int j = 0; j < kStage; ++j) n2[j] = 0.f;
   // the wave's 32-query group of operands: nks entries of 1 KiB
   const uint32_t gbytes = static_cast<uint32_t>(p.nks) * 1024u;
   const __amdgpu_buffer_rsrc_t ores = make_rsrc(static_cast<const char*>(p.qop) + g * gbytes, gbytes);
   const uint32_t lane_off = static_cast<uint32_t>(lane) * 16u;
 
-  floatx16 acc;
+  floatx16 acc[kRetBlocks];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int b = 0; b < kRetBlocks; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
 
-  int buf = 0;
-  for (int64_t fc = 0; fc < E; fc += kFC, buf ^= 1) {
-    const int nks = static_cast<int>((E - fc + 15) / 16 < kKS ? (E - fc + 15) / 16 : kKS);
-    const uint32_t ks0 = static_cast<uint32_t>(fc / 16);
-    // issue every load of the chunk before waiting on any: the key float4s
-    // (thread t takes row (t / 4) mod 32 and the float4 columns
-    // t mod 4 + 4 (t / 128) + 8 j, so four lanes read 64 contiguous bytes
-    // of a row and the wave covers 16 rows per load), then the wave's query
-    // operands (entries past the group's nks read as zero)
-    // prepared index: the chunk's tile is a contiguous run of nks x 64
-    // operand entries, already in the LDS order (swizzle included)
-    constexpr int kPK = kKS * 64 / 256;  // prepared entries per thread per chunk
-    halfx8 pk[PREP ? kPK : 1];
-    float4 kv[PREP ? 1 : kFC / 32];
-    if constexpr (PREP) {
-      const halfx8* src = static_cast<const halfx8*>(p.kop) +
-                          (static_cast<int64_t>(kb) * p.nks + fc / 16) * 64;
+  for (int64_t f0 = 0; f0 < E; f0 += kRound * kFC) {
+    if (f0 > 0) __syncthreads();  // the previous round's tiles have been read
+    // issue every load of the round: keys (prepared entries or fp32 rows),
+    // then the wave's query operands; entries past E or M read as zero
+    halfx8 pk[PREP ? kRound * kPK : 1];
+    float4 kv[PREP ? 1 : kRound * kStage];
 #pragma unroll
-      for (int j = 0; j < kPK; ++j) {
-        const int i = tid + 256 * j;
-        if (i < nks * 64) pk[j] = src[i];
-      }
-    } else {
+    for (int c = 0; c < kRound; ++c) {
+      const int64_t fc = f0 + c * kFC;
+      const int nks = fc < E ? static_cast<int>((E - fc + 15) / 16 < kKS ? (E - fc + 15) / 16 : kKS) : 0;
+      if constexpr (PREP) {
 #pragma unroll
-      for (int j = 0; j < kFC / 32; ++j) {
-        const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
-        const int64_t e = fc + 4 * c4;
-        const uint32_t off = e < E ? krow_off + static_cast<uint32_t>(e * 4) : kDropOffset;
-        kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
+        for (int j = 0; j < kPK; ++j) {
+          const int i = tid + kT * j;      // entry within the workgroup's chunk
+          const int b = i / (kKS * 64);    // block
+          const int w = i - b * (kKS * 64);
+          const int64_t kb = static_cast<int64_t>(kg) * kRetBlocks + b;
+          if (w < nks * 64 && kb < p.nkb)
+            pk[c * kPK + j] = static_cast<const halfx8*>(p.kop)[(kb * p.nks + fc / 16) * 64 + w];
+          else
+            pk[c * kPK + j] = halfx8{};
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < kStage; ++j) {
+          const int row = srow0 + (kT / kC4) * j;
+          const int64_t e = fc + 4 * c4;
+          const uint32_t off =
+              e < E ? static_cast<uint32_t>((row * E + e) * 4) : kDropOffset;
+          kv[c * kStage + j] =
+              __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
+        }
       }
     }
-    halfx8 aq[kKS];
+    halfx8 aq[kRound * kKS];
 #pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      const uint32_t so = (ks0 + ks) * 1024u;
-      aq[ks] = __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(ores, lane_off, so, 0));
+    for (int i = 0; i < kRound * kKS; ++i) {
+      const int64_t ks = f0 / 16 + i;
+      aq[i] = ks < p.nks ? __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(
+                                                          ores, lane_off,
+                                                          static_cast<uint32_t>(ks) * 1024u, 0))
+                         : halfx8{};
     }
-    if constexpr (PREP) {
-      halfx8* dst = &kop[buf][0][0][0];
 #pragma unroll
-      for (int j = 0; j < kPK; ++j) {
-        const int i = tid + 256 * j;
-        if (i < nks * 64) dst[i] = pk[j];
-      }
-    } else {
+    for (int c = 0; c < kRound; ++c) {
+      if constexpr (PREP) {
+        halfx8* dst = &kop[c][0][0][0][0];
 #pragma unroll
-      for (int j = 0; j < kFC / 32; ++j) {
-        const int c4 = (tid & 3) + 4 * (tid >> 7) + 8 * j;
-        const float4 v = kv[j];
-        n2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2))));
-        const int ks = c4 >> 2;
-        const int h = (c4 >> 1) & 1;
-        const int sub = c4 & 1;
-        const int srow = srow_base ^ ((2 * ks + h) & 31);
-        reinterpret_cast<halfx4*>(&kop[buf][ks][h][srow])[sub] = to_op(v);
+        for (int j = 0; j < kPK; ++j) dst[tid + kT * j] = pk[c * kPK + j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < kStage; ++j) {
+          const int row = srow0 + (kT / kC4) * j;
+          const float4 v = kv[c * kStage + j];
+          n2[j] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2[j]))));
+          const int b = row / kKB;
+          const int r = row % kKB;
+          const int ks = c4 >> 2;
+          const int h = (c4 >> 1) & 1;
+          const int sub = c4 & 1;
+          const int srow = r ^ ((2 * ks + h) & 31);
+          reinterpret_cast<halfx4*>(&kop[c][b][ks][h][srow])[sub] = to_op(v);
+        }
       }
     }
     __syncthreads();
     if (active) {
 #pragma unroll
-      for (int ks = 0; ks < kKS; ++ks) {
-        if (ks < nks) {
-          const int srow = r32 ^ ((2 * ks + half) & 31);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(aq[ks], kop[buf][ks][half][srow], acc, 0, 0, 0);
+      for (int c = 0; c < kRound; ++c) {
+#pragma unroll
+        for (int ks = 0; ks < kKS; ++ks) {
+          if (f0 + c * kFC + 16 * ks < E) {
+            const int srow = r32 ^ ((2 * ks + half) & 31);
+#pragma unroll
+            for (int b = 0; b < kRetBlocks; ++b)
+              acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kop[c][b][ks][half][srow],
+                                                              aq[c * kKS + ks], acc[b], 0, 0, 0);
+          }
         }
       }
     }
   }
   if (active) {
-    const int64_t key = k0 + r32;
-    const bool key_ok = key < p.M;
-    float mx[16];
+    const int64_t q = qw + r32;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      acc[r] *= kUnscale;
-      const int64_t q = qw + 8 * (r >> 2) + 4 * half + (r & 3);
-      if (q < p.Q && key_ok) p.scores[q * p.ld_scores + key] = acc[r];
-      mx[r] = key_ok ? acc[r] : -INFINITY;
-    }
-    // maximum over the 32 keys (lanes) of each half-wave, step-major so the
-    // 16 shuffles of a step are in flight together
-#pragma unroll
-    for (int m = 1; m < 32; m <<= 1) {
-      float t[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) t[r] = xor_shfl(mx[r], m);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx[r] = fmaxf(mx[r], t[r]);
-    }
-    if (r32 == 0) {
+    for (int b = 0; b < kRetBlocks; ++b) {
+      const int64_t kb = static_cast<int64_t>(kg) * kRetBlocks + b;
+      // largest (m1, its key i1) and the largest of the other keys (m2) over
+      // this lane's 16 rows; a tie with m1 goes to m2, keys past M rank last
+      float m1 = -INFINITY, m2 = -INFINITY;
+      int i1 = 0;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t q = qw + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (q < p.Q) p.blockmax[q * p.nkb + kb] = mx[r];
+        const int row = 8 * (r >> 2) + 4 * half + (r & 3);
+        const float v = kb * kKB + row < p.M ? acc[b][r] * kUnscale : -INFINITY;
+        if (v > m1) {
+          m2 = m1;
+          m1 = v;
+          i1 = row;
+        } else {
+          m2 = fmaxf(m2, v);
+        }
+      }
+      // merge with the other half's (rows 4 apart in each group of 8)
+      const float o1 = xor_shfl(m1, 32);
+      const float o2 = xor_shfl(m2, 32);
+      const int oi = __builtin_bit_cast(int, xor_shfl(__builtin_bit_cast(float, i1), 32));
+      const bool mine = m1 > o1 || (m1 == o1 && i1 < oi);
+      const float s1 = mine ? m1 : o1;
+      const float s2 = mine ? fmaxf(m2, o1) : fmaxf(o2, m1);
+      const int si = mine ? i1 : oi;
+      if (half == 0 && q < p.Q && kb < p.nkb) {
+        p.blockmax[q * p.nkb + kb] = s1;
+        p.blocksec[q * p.nkb + kb] = s2;
+        p.blockarg[q * p.nkb + kb] = static_cast<uint8_t>(si);
       }
     }
   }
   // squared key norms (workgroups with qg == 0; a prepared index holds
-  // them): the eight threads staging a row hold disjoint parts of it;
-  // combined in a fixed order
+  // them): the kC4 threads staging a row hold disjoint parts of it, adjacent
+  // lanes of one wave; combined in a fixed order
   if (!PREP && qg == 0) {
-    n2 += xor_shfl(n2, 1);
-    n2 += xor_shfl(n2, 2);
-    if ((tid & 3) == 0) nsum[tid >> 7][srow_base] = n2;
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) {
+      float v = n2[j];
+#pragma unroll
+      for (int m = 1; m < kC4; m <<= 1) v += xor_shfl(v, m);
+      if (c4 == 0) nsum[srow0 + (kT / kC4) * j] = v;
+    }
     __syncthreads();
-    if (tid < kKB) {
-      const float r2 = nsum[0][tid] + nsum[1][tid];
-      const bool ok = k0 + tid < p.M;
-      if (ok) p.rownorm2[k0 + tid] = r2;
-      float mx = ok ? r2 : 0.f;
+    if (tid < kRows) {
+      const int64_t key = k0 + tid;
+      if (key < p.M) p.rownorm2[key] = nsum[tid];
+    }
+    if (tid < kRetBlocks * kKB) {
+      const int64_t kb = static_cast<int64_t>(kg) * kRetBlocks + tid / kKB;
+      float mx = k0 + tid < p.M ? nsum[tid] : 0.f;
       mx = fmaxf(mx, xor_shfl(mx, 1));
       mx = fmaxf(mx, xor_shfl(mx, 2));
       mx = fmaxf(mx, xor_shfl(mx, 4));
       mx = fmaxf(mx, xor_shfl(mx, 8));
       mx = fmaxf(mx, xor_shfl(mx, 16));
-      if (tid == 0) p.blocknorm2[kb] = mx;
+      if ((tid & 31) == 0 && kb < p.nkb) p.blocknorm2[kb] = mx;
     }
   }
 }
@@ -361,7 +410,8 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   __shared__ int slot_i[64];
   const float4* qg4 = reinterpret_cast<const float4*>(p.q + q * p.E);
   const float* bm = p.blockmax + q * nkb;
-  const float* sc = p.scores + q * p.ld_scores;
+  const float* bsec = p.blocksec + q * nkb;
+  const uint8_t* barg = p.blockarg + q * nkb;
 
   // the block maxima and norms of the first kCacheGroups x 256 blocks,
   // loaded once (in flight with the query row) and held in registers for
@@ -582,41 +632,83 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
     ncand = 0;
   };
 
-  // surviving blocks go, in ascending order, to an LDS list whose keys are
-  // tested eight blocks per round (two per 64-lane pass, so their score and
-  // norm loads are in flight together), whatever 64-block slices they came
-  // from: a query whose few surviving blocks lie in different slices pays
-  // one round, not one per slice
+  // Surviving blocks go, in ascending order, to an LDS list, tested 64 per
+  // round (lane j takes entry i0 + j, its summary loads in flight together
+  // with the other lanes').  A key other than the block's largest has a
+  // screen score of at most the block's second largest, so if that second
+  // largest fails the test with the block's norm bound, the largest is the
+  // block's only candidate (tested with its own norm).  Otherwise every key
+  // of the block is rescored in fp32 from its fp32 row (lane l: key l mod 32,
+  // every other float4 of the features from l / 32 on, the two halves
+  // added): that sum differs from the exact score by at most
+  // gamma_{E+1} |q| |k_i|, far inside the screen's bound e(i), so the keys
+  // passing the same test with it are the block's candidates.
   int nbl = 0;
   auto test_list = [&]() __attribute__((always_inline)) {
     __syncthreads();  // the list entries written by other lanes are in
-    const int half = lane >> 5;
-    for (int i0 = 0; i0 < nbl; i0 += 8) {
-      int blk[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) blk[u] = i0 + u < nbl ? blist[i0 + u] : -1;
-      int64_t ii[4];
-      bool ok[4];
-      float sv[4], nv[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int b = half ? blk[2 * r + 1] : blk[2 * r];
-        ii[r] = static_cast<int64_t>(b) * kKB + (lane & (kKB - 1));
-        ok[r] = b >= 0 && ii[r] < p.M;
-        sv[r] = ok[r] ? sc[ii[r]] : 0.f;
-        nv[r] = ok[r] ? p.rownorm2[ii[r]] : 0.f;
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool cand_ok = ok[r] && (exhaustive || static_cast<double>(sv[r]) + err(nv[r]) >= thresh);
-        const uint64_t cmask = __ballot(cand_ok);
-        if (!cmask) continue;
+    for (int i0 = 0; i0 < nbl; i0 += 64) {
+      const bool on = i0 + lane < nbl;
+      const int kb = on ? blist[i0 + lane] : 0;
+      const float s1 = on ? bm[kb] : -INFINITY;
+      const float s2 = on ? bsec[kb] : -INFINITY;
+      const int a1 = on ? static_cast<int>(barg[kb]) : 0;
+      const float bn = on ? p.blocknorm2[kb] : 0.f;
+      const int64_t key1 = static_cast<int64_t>(kb) * kKB + a1;
+      const bool key_ok = on && key1 < p.M;
+      const float kn = key_ok ? p.rownorm2[key1] : 0.f;
+      const bool full = on && (exhaustive || static_cast<double>(s2) + err(bn) >= thresh);
+      const bool single =
+          key_ok && !full && static_cast<double>(s1) + err(kn) >= thresh;
+      const uint64_t smask = __ballot(single);
+      if (smask) {
         if (ncand + 64 > kCand) {
           early = true;
           flush();
         }
-        if (cand_ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(ii[r]);
-        ncand += __builtin_popcountll(cmask);
+        if (single) cand[ncand + __builtin_popcountll(smask & ((1ull << lane) - 1))] = static_cast<int>(key1);
+        ncand += __builtin_popcountll(smask);
+      }
+      uint64_t fmask = __ballot(full);
+      while (fmask) {
+        const int j = __builtin_ctzll(fmask);
+        fmask &= fmask - 1;
+        const int64_t b0 = static_cast<int64_t>(__builtin_amdgcn_readlane(kb, j)) * kKB;
+        const int cnt = static_cast<int>(p.M - b0 < kKB ? p.M - b0 : kKB);
+        const int r = lane & (kKB - 1);
+        const bool kok = r < cnt;
+        float part[4] = {0.f, 0.f, 0.f, 0.f};
+        if (kok) {
+          const float4* row = reinterpret_cast<const float4*>(p.K + (b0 + r) * p.E);
+          for (int e4 = lane >> 5; e4 < e4n; e4 += 8) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int f = e4 + 2 * u;
+              if (f < e4n) {
+                const float4 v = row[f];
+                const double2 q01 = *reinterpret_cast<const double2*>(qs + 4 * f);
+                const double2 q23 = *reinterpret_cast<const double2*>(qs + 4 * f + 2);
+                part[u] = fmaf(static_cast<float>(q01.x), v.x, part[u]);
+                part[u] = fmaf(static_cast<float>(q01.y), v.y, part[u]);
+                part[u] = fmaf(static_cast<float>(q23.x), v.z, part[u]);
+                part[u] = fmaf(static_cast<float>(q23.y), v.w, part[u]);
+              }
+            }
+          }
+        }
+        float tot = (part[0] + part[1]) + (part[2] + part[3]);
+        tot += xor_shfl(tot, 32);
+        const bool ok = lane < kKB && kok &&
+                        (exhaustive || static_cast<double>(tot) +
+                                           err(p.rownorm2[b0 + r]) >= thresh);
+        const uint64_t cmask = __ballot(ok);
+        if (cmask) {
+          if (ncand + kKB > kCand) {
+            early = true;
+            flush();
+          }
+          if (ok) cand[ncand + __builtin_popcountll(cmask & ((1ull << lane) - 1))] = static_cast<int>(b0 + r);
+          ncand += __builtin_popcountll(cmask);
+        }
       }
     }
     __syncthreads();  // every list entry is read before the list is refilled
@@ -714,12 +806,13 @@ hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s) {
   if (p.nkb > 0) {
     const int64_t entries = static_cast<int64_t>(p.nqg) * p.nks * 64;
     hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, s, p);
-    const int64_t nqwg = (p.Q + kQWG - 1) / kQWG;
-    const dim3 grid(static_cast<unsigned>(p.nkb * nqwg));
+    const int64_t nqwg = (p.Q + 32 * kRetWaves - 1) / (32 * kRetWaves);
+    const int64_t nkbg = (p.nkb + kRetBlocks - 1) / kRetBlocks;
+    const dim3 grid(static_cast<unsigned>(nkbg * nqwg));
     if (p.kop != nullptr)
-      hipLaunchKernelGGL(screen_kernel<true>, grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL(screen_kernel<true>, grid, dim3(64 * kRetWaves), 0, s, p);
     else
-      hipLaunchKernelGGL(screen_kernel<false>, grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL(screen_kernel<false>, grid, dim3(64 * kRetWaves), 0, s, p);
   }
   hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
   return hipGetLastError();

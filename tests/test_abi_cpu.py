@@ -142,7 +142,9 @@ def test_chunk_cap_covers_the_coefficient_streams():
 def test_retrieve_validation_errors():
     L = P.lib()
     ws = P.retrieve_workspace_bytes(4, 10, 16)
-    assert ws >= 4 * 10 * 4 + 10 * 4
+    assert ws >= 4 * 9 + 10 * 4
+    # the workspace scales with Q M / 32 (block summaries), not with Q M
+    assert P.retrieve_workspace_bytes(256, 10000, 384) < 256 * 10000 * 4 // 8
     call = lambda q=FAKE, k=FAKE, Q=4, M=10, E=16, idx=FAKE, w=FAKE, wb=ws: \
         L.precog_retrieve_top1(q, k, Q, M, E, idx, w, wb, None)
     assert call(Q=-1) == ESHAPE

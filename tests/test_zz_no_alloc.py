@@ -61,11 +61,14 @@ def test_noalloc_matches_workspace_entry_point_twice():
 
 
 def test_noalloc_rejects_workspace_past_the_array():
-    # 4 Q M bytes of screen scores alone exceed the 32 MiB array
-    q = torch.zeros((4096, 64), dtype=torch.float32, device=DEV)
-    K = torch.zeros((10000, 64), dtype=torch.float32, device=DEV)
-    idx = torch.full((4096,), -7, dtype=torch.int32, device=DEV)
-    st = P.lib().precog_retrieve_top1_noalloc(q.data_ptr(), K.data_ptr(), 4096, 10000, 64,
+    # the block summaries of 16384 queries x 100,000 keys (9 bytes per query
+    # and 32-key block, 460 MB) exceed the 32 MiB array
+    Q, M = 16384, 100000
+    assert P.retrieve_workspace_bytes(Q, M, 64) > P.NOALLOC_SCRATCH_BYTES
+    q = torch.zeros((Q, 64), dtype=torch.float32, device=DEV)
+    K = torch.zeros((M, 64), dtype=torch.float32, device=DEV)
+    idx = torch.full((Q,), -7, dtype=torch.int32, device=DEV)
+    st = P.lib().precog_retrieve_top1_noalloc(q.data_ptr(), K.data_ptr(), Q, M, 64,
                                               idx.data_ptr(), None)
     assert st == 6  # PRECOG_ERR_WORKSPACE
     torch.cuda.synchronize()
