@@ -662,6 +662,26 @@ def bench_extensions(args, flush):
                              **rates(scan_bytes(B, L, D, N) + B * D * N * 2, x_ms)}
     del inp, y, hT, A_im
     torch.cuda.empty_cache()
+
+    # complex-A scan on the long-context shape, in 256-token chunks
+    wl = synth.LONG_CONTEXT
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed, torch.bfloat16)
+    A_im = synth.complex_frequencies(D, N).cuda()
+    y = torch.empty((B, L, D), dtype=torch.bfloat16, device="cuda")
+    hT = torch.empty((B, D, N, 2), dtype=torch.float16, device="cuda")
+    desc = P.scan_desc(B, L, D, N, P.BF16, P.BF16, P.F16, chunk=wl.chunk)
+    nws = P.scan_complex_workspace_bytes(desc)
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    run = lambda: P.scan_complex_raw(desc, inp["x"], inp["dt"], inp["A"], A_im, inp["B"],
+                                     inp["C"], inp["z"], inp["Dskip"], None, y, hT, ws, nws)
+    x_ms = time_events(run, 5)
+    res["complex_long_context"] = {"workload": wl.name + ", w_n = pi n, fp16 complex hT",
+                                   "ms": x_ms, "tokens_per_s": B * L / (x_ms * 1e-3),
+                                   "workspace_bytes": nws,
+                                   **rates(scan_bytes(B, L, D, N) + B * D * N * 2, x_ms)}
+    del inp, y, hT, A_im, ws
+    torch.cuda.empty_cache()
     return res
 
 

@@ -206,16 +206,27 @@ precog_status precog_scan_trajectory(const precog_scan_desc *desc,
  *   A_re, A_im  [D, N] fp32; A_re > 0.
  *   h0, hT      complex state rows [D, N, 2] ((real, imaginary) interleaved)
  *               in desc->state_dtype; batch strides in elements, 0 = 2*D*N.
- *   desc->dstate in {1, 2, 4, 8, 16}; one pass over the sequence
- *               (desc->chunk 0 or >= L), so no workspace.
+ *   desc->dstate in {1, 2, 4, 8, 16}.
+ *   Time chunks as in precog_scan_encode (desc->chunk, 0 = automatic: one
+ *               pass when batch x channels fill the GPU; chunks are capped
+ *               so that chunk * max(D, N) * 4 < 2^31).  A chunked scan folds
+ *               the chunks' end states with the product of their decays,
+ *               exp(-(A_re + i A_im) sum dt) (its angle reduced in fp64),
+ *               and replays each chunk from its carried-in state.
+ *   workspace   precog_scan_complex_workspace_bytes(desc) bytes (0 for one
+ *               pass: NULL allowed), 16-byte aligned; about
+ *               B * chunks * D * (8 N + 4) bytes.
  * The rotation uses the hardware sine and cosine of the angle reduced to
  * [0, 1) revolutions; the magnitude uses the hardware exp2. */
+size_t precog_scan_complex_workspace_bytes(const precog_scan_desc *desc);
+
 precog_status precog_scan_complex(const precog_scan_desc *desc, const void *x,
                                   const void *dt, const float *A_re,
                                   const float *A_im, const void *B,
                                   const void *C, const void *z,
                                   const float *Dskip, const void *h0, void *y,
-                                  void *hT, void *stream);
+                                  void *hT, void *workspace,
+                                  size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Cosine top-1 retrieval                                                   */

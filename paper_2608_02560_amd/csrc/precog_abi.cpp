@@ -603,30 +603,64 @@ precog_status precog_smc_consolidate(void* states, precog_dtype state_dtype, int
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 
-precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, const void* dt,
-                                  const float* A_re, const float* A_im, const void* B,
-                                  const void* C, const void* z, const float* Dskip,
-                                  const void* h0, void* y, void* hT, void* stream) {
-  precog_status st = validate_desc(desc);
+namespace {
+// Complex-A validation shared by the entry point and its workspace query:
+// N <= 16, state strides counted in (re, im) pairs.
+precog_status validate_complex_desc(const precog_scan_desc* desc) {
+  const precog_status st = validate_desc(desc);
   if (st != PRECOG_OK) return st;
-  const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
-  if (N > 16) return PRECOG_ERR_SHAPE;
-  if (desc->chunk != 0 && desc->chunk < L) return PRECOG_ERR_SHAPE;  // one pass only
-  const int64_t dn2 = 2 * D * N;
+  if (desc->dstate > 16) return PRECOG_ERR_SHAPE;
+  const int64_t dn2 = 2 * desc->dim * desc->dstate;
   if ((desc->h0_batch_stride != 0 && desc->h0_batch_stride < dn2) ||
       (desc->hT_batch_stride != 0 && desc->hT_batch_stride < dn2))
     return PRECOG_ERR_STRIDE;
+  return PRECOG_OK;
+}
+
+// Complex-A workspace: carries [B, C, D, N, 2] fp32 and chunk dt sums
+// [B, C, D] fp32, each 256-byte aligned.
+ScanWs complex_ws(const precog_scan_desc* d, int64_t nchunks) {
+  ScanWs w{0, 0, 0};
+  if (nchunks <= 1) return w;
+  w.carry_bytes = align_up(static_cast<size_t>(d->batch) * nchunks * d->dim * d->dstate * 2 * 4);
+  w.dtsum_bytes = align_up(static_cast<size_t>(d->batch) * nchunks * d->dim * 4);
+  w.total = w.carry_bytes + w.dtsum_bytes;
+  return w;
+}
+}  // namespace
+
+size_t precog_scan_complex_workspace_bytes(const precog_scan_desc* desc) {
+  if (validate_complex_desc(desc) != PRECOG_OK) return 0;
+  const int64_t ch = effective_chunk(desc);
+  const int64_t nch = desc->seqlen > 0 ? ceil_div(desc->seqlen, ch) : 1;
+  return complex_ws(desc, nch).total;
+}
+
+precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, const void* dt,
+                                  const float* A_re, const float* A_im, const void* B,
+                                  const void* C, const void* z, const float* Dskip,
+                                  const void* h0, void* y, void* hT, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  precog_status st = validate_complex_desc(desc);
+  if (st != PRECOG_OK) return st;
+  const int64_t Bt = desc->batch, L = desc->seqlen, D = desc->dim, N = desc->dstate;
   if (Bt == 0 || D == 0) return PRECOG_OK;
   const bool work = L > 0;
   if (!A_re || !A_im) return PRECOG_ERR_NULL;
   if (work && (!x || !dt || !B)) return PRECOG_ERR_NULL;
   if (work && y && !C) return PRECOG_ERR_NULL;
   if ((!y || !work) && !hT) return PRECOG_OK;  // nothing requested
-  const void* ptrs[] = {x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT};
+  const void* ptrs[] = {x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT, workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  const int64_t chunk = effective_chunk(desc);
+  const int64_t nchunks = work ? ceil_div(L, chunk) : 1;
+  if (nchunks > (1LL << 20)) return PRECOG_ERR_SHAPE;
+  const ScanWs ws = complex_ws(desc, nchunks);
+  if (ws.total > 0 && (!workspace || workspace_bytes < ws.total)) return PRECOG_ERR_WORKSPACE;
   const int64_t dblocks = ceil_div(D, kBlock);
-  if (dblocks * Bt > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (dblocks * Bt * nchunks > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  if (Bt * D * N / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   int cus = 1;
   st = check_device(&cus);
   if (st != PRECOG_OK) return st;
@@ -643,19 +677,23 @@ precog_status precog_scan_complex(const precog_scan_desc* desc, const void* x, c
   p.h0 = h0;
   p.y = work ? y : nullptr;
   p.hT = hT;
+  p.carry = ws.total ? static_cast<float*>(workspace) : nullptr;
+  p.dtsum = ws.total ? reinterpret_cast<float*>(static_cast<char*>(workspace) + ws.carry_bytes)
+                     : nullptr;
   p.B = Bt;
   p.L = L;
   p.D = D;
-  p.chunk = L;
-  p.h0_stride = desc->h0_batch_stride ? desc->h0_batch_stride : dn2;
-  p.hT_stride = desc->hT_batch_stride ? desc->hT_batch_stride : dn2;
-  p.nchunks = 1;
+  p.chunk = chunk;
+  p.h0_stride = desc->h0_batch_stride ? desc->h0_batch_stride : 2 * D * N;
+  p.hT_stride = desc->hT_batch_stride ? desc->hT_batch_stride : 2 * D * N;
+  p.nchunks = static_cast<int>(nchunks);
   p.dblocks = static_cast<int>(dblocks);
   p.flags = (p.z ? precog::kHasZ : 0) | (p.Dskip ? precog::kHasD : 0) |
             (h0 ? precog::kHasH0 : 0) | (hT ? precog::kHasHT : 0);
-  // progress balancing when every wave is resident from the start (as for
-  // the real-A scan)
-  if (dblocks * Bt * (kBlock / 64) <= 4LL * 4 * cus) p.flags |= precog::kBalance;
+  // progress balancing when every wave of the final pass is resident from
+  // the start (as for the real-A scan)
+  if (dblocks * Bt * nchunks * (kBlock / 64) <= 4LL * 4 * cus) p.flags |= precog::kBalance;
+  if (!p.y && !p.hT) return PRECOG_OK;  // L == 0 and no state requested
   (void)hipGetLastError();
   const hipError_t e = precog::launch_scan_complex(p, static_cast<int>(N), desc->in_dtype,
                                                    desc->out_dtype, desc->state_dtype,

@@ -39,7 +39,8 @@ struct ScanParams {
   double h0_inv_tau;        // 1 / temperature of that composition
   void* y;
   void* hT;
-  float* carry;   // [B, C, D, N] fp32: slot 0 = h0, slot c = state entering chunk c
+  float* carry;   // [B, C, D, N] fp32 ([B, C, D, N, 2] for complex A): slot 0 = h0,
+                  // slot c = state entering chunk c
   float* dtsum;   // [B, C, D] fp32: slot c = sum of dt over chunk c (c < C-1)
   void* traj;     // [B, traj_count, D, N] state dtype (trajectory launches only)
   int64_t traj_every, traj_count;
@@ -62,7 +63,8 @@ hipError_t launch_scan(const ScanParams& p, int N, int in_dtype, int out_dtype,
                        int state_dtype, hipStream_t s);
 hipError_t launch_scan_traj(const ScanParams& p, int N, int in_dtype, int out_dtype,
                             int state_dtype, hipStream_t s);
-// Complex diagonal A: one pass, N <= 16, states interleaved (re, im).
+// Complex diagonal A: N <= 16, states interleaved (re, im); chunked like the
+// real scan (summary, carry fold, replay) when p.nchunks > 1.
 hipError_t launch_scan_complex(const ScanParams& p, int N, int in_dtype, int out_dtype,
                                int state_dtype, hipStream_t s);
 

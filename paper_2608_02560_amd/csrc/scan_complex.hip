@@ -7,11 +7,22 @@
 //
 // Same work decomposition as the real scan (one lane per (b, d) channel, 64
 // adjacent channels per wave, buffer loads, B_t / C_t reaching every lane as
-// DPP row_newbcast operands), one pass over the whole sequence.  Per
-// (t, d, n): exp2 of dt a' for the magnitude; the angle dt w / (2 pi) in
-// revolutions, reduced to [0, 1) by v_fract_f32, then v_cos_f32 / v_sin_f32
-// (which take revolutions); then the complex multiply-add
+// DPP row_newbcast operands).  Per (t, d, n): exp2 of dt a' for the
+// magnitude; the angle dt w / (2 pi) in revolutions, reduced to [0, 1) by
+// v_fract_f32, then v_cos_f32 / v_sin_f32 (which take revolutions); then the
+// complex multiply-add
 //   re' = c re + s im + B u,   im' = c im - s re,   (c, s) = |decay| (cos, sin).
+//
+// Long sequences over few channels are cut into time chunks as in the real
+// scan (two levels):
+//   pass 1 (summary): each chunk but the last is scanned from a zero state;
+//          its complex end state and its sum of dt go to the workspace;
+//   pass 2 (carry):   per (b, d, n), H_c = exp(-S_{c-1} (a + i w)) H_{c-1}
+//          + s_{c-1}, sequential over chunks: the composition of the affine
+//          maps h -> r h + s that each chunk applies, whose factor is the
+//          product of its tokens' decays, exp(-(a + i w) sum dt);
+//   pass 3 (replay):  each chunk is rescanned from its carried-in state,
+//          producing y and, for the last chunk, hT.
 #include "scan_kernels.h"
 
 namespace precog {
@@ -19,7 +30,7 @@ namespace {
 
 constexpr float kInv2Pi = 0.15915494309189535f;
 
-template <int N, bool READOUT, int... m>
+template <int N, int... m>
 __device__ __forceinline__ void ctoken(float (&hr)[N], float (&hi)[N], const float (&a2)[N],
                                        const float (&w1)[N], float dtv, float u, float bv,
                                        std::integer_sequence<int, m...>) {
@@ -54,17 +65,22 @@ __device__ __forceinline__ void store_cstate(TSt* dst, const float (&hr)[N], con
   store_state_vec<2 * N>(dst, v);
 }
 
-// One lane = one (b, d) channel over the whole sequence.  READOUT: y is
-// written (else state only); HASZ: gate present.
-template <int N, typename TIn, typename TOut, typename TSt, bool READOUT, bool HASZ>
+// One lane = one (b, d) channel over one time chunk.  HASZ: gate present.
+//   KIND == kReadout:   y and (last chunk) hT
+//   KIND == kStateOnly: hT only (y == NULL: C, z, Dskip unread)
+//   KIND == kSummary:   chunk end state from zero -> carry slot c+1, sum dt
+template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ>
 __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
     const ScanParams p) {
   constexpr int kPer = N < 16 ? N : 16;
+  constexpr bool kRead = KIND == kReadout;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int dblk = lb % p.dblocks;
-  const int b = lb / p.dblocks;
+  const int rest = lb / p.dblocks;
+  const int b = rest % static_cast<int>(p.B);
+  const int c = rest / static_cast<int>(p.B);
   const int64_t D = p.D;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -77,7 +93,10 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
   const int64_t dtrue = wave_d0 + lane;
   const bool live = dtrue < D;
   const int64_t d = live ? dtrue : D - 1;
-  const int nsteps = static_cast<int>(p.L);
+
+  const int64_t t0 = static_cast<int64_t>(c) * p.chunk;
+  const int64_t t1 = min(p.L, t0 + p.chunk);
+  const int nsteps = static_cast<int>(t1 > t0 ? t1 - t0 : 0);
 
   float a2[N], w1[N];
   load_state<N>(a2, p.A + d * N);
@@ -87,18 +106,27 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
     a2[n] *= -kLog2e;
     w1[n] *= kInv2Pi;
   }
+  // carry slots hold (re, im) pairs: [B, C, D, N, 2]
+  const int64_t DN2 = 2 * D * N;
   float hr[N], hi[N];
-  if (p.flags & kHasH0) {
+  if constexpr (KIND == kSummary) {
+#pragma unroll
+    for (int n = 0; n < N; ++n) hr[n] = hi[n] = 0.f;
+  } else if (p.nchunks > 1) {
+    load_cstate<N>(hr, hi, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * DN2 + 2 * d * N);
+  } else if (p.flags & kHasH0) {
     load_cstate<N>(hr, hi, static_cast<const TSt*>(p.h0) + b * p.h0_stride + 2 * d * N);
   } else {
 #pragma unroll
     for (int n = 0; n < N; ++n) hr[n] = hi[n] = 0.f;
   }
-  const float dsk = (READOUT && (p.flags & kHasD)) ? p.Dskip[d] : 0.f;
+  const float dsk = (kRead && (p.flags & kHasD)) ? p.Dskip[d] : 0.f;
 
+  // descriptors over this chunk's rows of x, dt, z, y ([nsteps, D]) and B, C
+  // ([nsteps, N]); lane offsets in bytes
   using SI = Stream<TIn>;
   using SO = Stream<TOut>;
-  const int64_t row0 = static_cast<int64_t>(b) * p.L;
+  const int64_t row0 = static_cast<int64_t>(b) * p.L + t0;
   const uint32_t in_row = static_cast<uint32_t>(D * sizeof(TIn));
   const uint32_t out_row = static_cast<uint32_t>(D * sizeof(TOut));
   const uint32_t bc_row = static_cast<uint32_t>(N * sizeof(TIn));
@@ -130,15 +158,16 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
       if constexpr (HASZ) tb.z[k] = SI::load(rz, dl, so);
       const uint32_t sb = static_cast<uint32_t>(st) * bc_row;
       tb.b[k] = SI::load(rb, el, sb);
-      if constexpr (READOUT) tb.c[k] = SI::load(rc, el, sb);
+      if constexpr (kRead) tb.c[k] = SI::load(rc, el, sb);
     }
   };
+  float dtacc = 0.f;
   auto step = [&](const Tile& tb, int k, int st) {
     const float xv = SI::f32(tb.x[k]);
     const float dtv = SI::f32(tb.dt[k]);
     const float u = dtv * xv;
-    ctoken<N, READOUT>(hr, hi, a2, w1, dtv, u, SI::f32(tb.b[k]), std::make_integer_sequence<int, kPer>{});
-    if constexpr (READOUT) {
+    ctoken<N>(hr, hi, a2, w1, dtv, u, SI::f32(tb.b[k]), std::make_integer_sequence<int, kPer>{});
+    if constexpr (kRead) {
       float acc = 0.f;
       readout_group<N, 0>(acc, SI::f32(tb.c[k]), hr);
       float out = fmaf(dsk, xv, acc);
@@ -149,6 +178,7 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
       }
       SO::store(ry, dly, static_cast<uint32_t>(st) * out_row, out);
     }
+    if constexpr (KIND == kSummary) dtacc += dtv;
   };
   auto run_tile = [&](const Tile& tb, int tile) {
 #pragma unroll
@@ -177,26 +207,98 @@ __global__ __launch_bounds__(kSBlock) void scan_complex_kernel(
   }
 
   if (!live) return;
-  if (p.flags & kHasHT) store_cstate<N>(static_cast<TSt*>(p.hT) + b * p.hT_stride + 2 * d * N, hr, hi);
+  if constexpr (KIND == kSummary) {
+    store_cstate<N>(p.carry + (static_cast<int64_t>(b) * p.nchunks + c + 1) * DN2 + 2 * d * N, hr,
+                    hi);
+    p.dtsum[(static_cast<int64_t>(b) * p.nchunks + c) * D + d] = dtacc;
+  } else {
+    if ((p.flags & kHasHT) && c == p.nchunks - 1)
+      store_cstate<N>(static_cast<TSt*>(p.hT) + b * p.hT_stride + 2 * d * N, hr, hi);
+  }
+}
+
+// Pass 2: per (b, d, n) lane, fold the chunk summaries in time order.
+// carry[b, 0] = h0; carry[b, c] = exp(-S_{c-1} (a + i w)) carry[b, c-1]
+// + s_{c-1}, where pass 1 left s_{c-1} in carry[b, c] and S_{c-1} in
+// dtsum[b, c-1].  The magnitude is exp2(a' S) as in the tokens; the angle
+// S w / (2 pi) is formed and reduced to [0, 1) revolutions in fp64 (it
+// reaches hundreds of revolutions over a long chunk, where fp32 would keep
+// too few fraction bits), then cos / sin as in the tokens.
+template <typename TSt>
+__global__ __launch_bounds__(256) void complex_carry_kernel(const ScanParams p, int N) {
+  const int64_t DN = p.D * N;
+  const int64_t gid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (gid >= p.B * DN) return;
+  const int64_t b = gid / DN;
+  const int64_t dn = gid - b * DN;
+  const int64_t d = dn / N;
+  const float a2 = -kLog2e * p.A[dn];
+  const double w1 = static_cast<double>(p.A_im[dn]) * 0.15915494309189535;  // 1 / (2 pi)
+  float Hr = 0.f, Hi = 0.f;
+  if (p.flags & kHasH0) {
+    const TSt* src = static_cast<const TSt*>(p.h0) + b * p.h0_stride + 2 * dn;
+    Hr = to_f32(src[0]);
+    Hi = to_f32(src[1]);
+  }
+  float* cp = p.carry + b * p.nchunks * 2 * DN + 2 * dn;
+  const float* sp = p.dtsum + b * p.nchunks * p.D + d;
+  cp[0] = Hr;
+  cp[1] = Hi;
+  constexpr int kU = 4;
+  for (int c0 = 1; c0 < p.nchunks; c0 += kU) {
+    float sr[kU], si[kU], Sv[kU];
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      if (c0 + k < p.nchunks) {
+        sr[k] = cp[(c0 + k) * 2 * DN];
+        si[k] = cp[(c0 + k) * 2 * DN + 1];
+        Sv[k] = sp[(c0 + k - 1) * p.D];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kU; ++k) {
+      if (c0 + k < p.nchunks) {
+        const double turns = static_cast<double>(Sv[k]) * w1;
+        const float rev = static_cast<float>(turns - floor(turns));
+        const float mag = __builtin_amdgcn_exp2f(a2 * Sv[k]);
+        const float cs = mag * __builtin_amdgcn_cosf(rev);
+        const float sn = mag * __builtin_amdgcn_sinf(rev);
+        const float re = Hr;
+        Hr = fmaf(cs, re, fmaf(sn, Hi, sr[k]));
+        Hi = fmaf(cs, Hi, fmaf(-sn, re, si[k]));
+        cp[(c0 + k) * 2 * DN] = Hr;
+        cp[(c0 + k) * 2 * DN + 1] = Hi;
+      }
+    }
+  }
 }
 
 template <int N, typename TIn, typename TOut, typename TSt>
 hipError_t launch_c(const ScanParams& p, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(p.dblocks) * p.B));
+  const int64_t rows_blocks = static_cast<int64_t>(p.dblocks) * p.B;
   const TIn* X = static_cast<const TIn*>(p.x);
   const TIn* DT = static_cast<const TIn*>(p.dt);
   const TIn* Z = static_cast<const TIn*>(p.z);
   const TIn* BB = static_cast<const TIn*>(p.Bm);
   const TIn* CC = static_cast<const TIn*>(p.Cm);
+  if (p.nchunks > 1) {
+    const dim3 g1(static_cast<unsigned>(rows_blocks * (p.nchunks - 1)));
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, float, float, kSummary, false>), g1,
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
+    const int64_t lanes = p.B * p.D * N;
+    hipLaunchKernelGGL((complex_carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)),
+                       dim3(256), 0, s, p, N);
+  }
+  const dim3 grid(static_cast<unsigned>(rows_blocks * p.nchunks));
   if (p.y != nullptr && (p.flags & kHasZ))
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, true>), grid, dim3(kSBlock), 0, s,
-                       X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, kReadout, true>), grid, dim3(kSBlock),
+                       0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else if (p.y != nullptr)
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, true, false>), grid, dim3(kSBlock), 0, s,
-                       X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, TOut, TSt, kReadout, false>), grid,
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
   else
-    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, float, TSt, false, false>), grid, dim3(kSBlock), 0, s,
-                       X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
+    hipLaunchKernelGGL((scan_complex_kernel<N, TIn, float, TSt, kStateOnly, false>), grid,
+                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
   return hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ STATUS = {0: "PRECOG_OK", 1: "PRECOG_ERR_NULL", 2: "PRECOG_ERR_SHAPE", 3: "PRECO
 
 EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_encode_indexed",
            "precog_scan_trajectory",
-           "precog_scan_complex",
+           "precog_scan_complex", "precog_scan_complex_workspace_bytes",
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
            "precog_retrieve_top1_noalloc",
            "precog_retrieve_topk", "precog_retrieve_index_bytes", "precog_retrieve_prepare",
@@ -72,8 +72,10 @@ def lib():
         L.precog_scan_trajectory.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 11 + \
             [i64, vp, sz, vp]
         L.precog_scan_trajectory.restype = ctypes.c_int
-        L.precog_scan_complex.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 12
+        L.precog_scan_complex.argtypes = [ctypes.POINTER(ScanDesc)] + [vp] * 12 + [sz, vp]
         L.precog_scan_complex.restype = ctypes.c_int
+        L.precog_scan_complex_workspace_bytes.argtypes = [ctypes.POINTER(ScanDesc)]
+        L.precog_scan_complex_workspace_bytes.restype = sz
         L.precog_retrieve_workspace_bytes.argtypes = [i64, i64, i64]
         L.precog_retrieve_workspace_bytes.restype = sz
         L.precog_retrieve_top1.argtypes = [vp, vp, i64, i64, i64, vp, vp, sz, vp]
@@ -172,12 +174,17 @@ def scan_trajectory(desc: ScanDesc, x, dt, A, B, C=None, z=None, Dskip=None, h0=
     _check("precog_scan_trajectory", st)
 
 
+def scan_complex_workspace_bytes(desc: ScanDesc) -> int:
+    return int(lib().precog_scan_complex_workspace_bytes(ctypes.byref(desc)))
+
+
 def scan_complex_raw(desc: ScanDesc, x, dt, A_re, A_im, B, C=None, z=None, Dskip=None, h0=None,
-                     y=None, hT=None, stream=None):
+                     y=None, hT=None, workspace=None, workspace_bytes=0, stream=None):
     """precog_scan_complex on device tensors (or raw device pointers)."""
     st = lib().precog_scan_complex(ctypes.byref(desc), _ptr(x), _ptr(dt), _ptr(A_re), _ptr(A_im),
                                    _ptr(B), _ptr(C), _ptr(z), _ptr(Dskip), _ptr(h0), _ptr(y),
-                                   _ptr(hT), _stream(stream))
+                                   _ptr(hT), _ptr(workspace), int(workspace_bytes),
+                                   _stream(stream))
     _check("precog_scan_complex", st)
 
 
@@ -342,14 +349,16 @@ def trajectory(x, dt, A, B, every, C=None, z=None, Dskip=None, h0=None, *,
 
 def scan_complex(x, dt, A_re, A_im, B, C=None, z=None, Dskip=None, h0=None, *,
                  out_dtype=torch.float32, state_dtype=torch.float32, want_y=True, want_hT=True,
-                 stream=None):
+                 chunk=0, stream=None):
     """Complex-A scan; returns (y, hT) with hT [Bt, D, N, 2] (None where not requested)."""
     Bt, L, D = x.shape
     N = A_re.shape[1]
-    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[state_dtype])
+    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[state_dtype], chunk=chunk)
     y = torch.empty((Bt, L, D), dtype=out_dtype, device=x.device) if want_y else None
     hT = torch.empty((Bt, D, N, 2), dtype=state_dtype, device=x.device) if want_hT else None
-    scan_complex_raw(desc, x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT, stream)
+    nbytes = scan_complex_workspace_bytes(desc)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    scan_complex_raw(desc, x, dt, A_re, A_im, B, C, z, Dskip, h0, y, hT, ws, nbytes, stream)
     return y, hT
 
 

@@ -182,17 +182,38 @@ def test_trajectory_validation_errors():
 def test_complex_scan_validation_errors():
     L = P.lib()
 
-    def call(desc, x=FAKE, Aim=FAKE, h0=None):
+    def call(desc, x=FAKE, Aim=FAKE, h0=None, ws=None, wsb=0):
         return L.precog_scan_complex(ctypes.byref(desc), x, FAKE, FAKE, Aim, FAKE, FAKE, FAKE,
-                                     FAKE, h0, FAKE, FAKE, None)
+                                     FAKE, h0, FAKE, FAKE, ws, wsb, None)
     assert call(P.scan_desc(2, 16, 64, 32)) == ESHAPE          # N > 16
-    assert call(P.scan_desc(2, 16, 64, 16, chunk=8)) == ESHAPE  # one pass only
     assert call(P.scan_desc(2, 16, 64, 16, h0_batch_stride=64 * 16)) == ESTRIDE  # < 2 D N
     assert call(P.scan_desc(2, 16, 64, 16), Aim=None) == ENULL
     assert call(P.scan_desc(2, 16, 64, 16), x=None) == ENULL
     assert call(P.scan_desc(2, 16, 60, 16)) == EALIGN
     assert call(P.scan_desc(2, 16, 64, 16), h0=FAKE + 4) == EALIGN
     assert call(P.scan_desc(0, 16, 64, 16)) == OK
+    # chunked complex scans need workspace: carries [B, C, D, N, 2] fp32 and
+    # chunk dt sums [B, C, D] fp32, each 256-byte aligned
+    chunked = P.scan_desc(2, 1024, 64, 16, chunk=128)
+    need = P.scan_complex_workspace_bytes(chunked)
+    assert need == 2 * 8 * 64 * 16 * 2 * 4 + 2 * 8 * 64 * 4
+    assert call(chunked) == EWS
+    assert call(chunked, ws=FAKE, wsb=need - 1) == EWS
+    assert call(chunked, ws=FAKE + 8, wsb=need) == EALIGN
+    assert P.scan_complex_workspace_bytes(P.scan_desc(2, 1024, 64, 16, chunk=1024)) == 0
+    assert P.scan_complex_workspace_bytes(P.scan_desc(2, 1024, 64, 32)) == 0  # invalid: N > 16
+
+
+def test_complex_chunk_cap_keeps_32bit_offsets():
+    """A one-chunk request whose per-token streams would pass 2^31 bytes
+    (70,000 tokens x 8200 channels x 4 bytes) is cut at
+    (2^31 - 1) / (8200 * 4) = 65,472 tokens into two chunks, so it takes a
+    workspace instead of wrapping the kernels' 32-bit offsets."""
+    L = 70000
+    d = P.scan_desc(1, L, 8200, 16, in_dtype=P.F32, out_dtype=P.F32, chunk=L)
+    cap = (2 ** 31 - 1) // (8200 * 4)
+    assert cap == 65472 and -(-L // cap) == 2
+    assert P.scan_complex_workspace_bytes(d) == 2 * 8200 * 16 * 2 * 4 + 2 * 8200 * 4 + 192
 
 
 def test_topk_validation_errors():

@@ -1,8 +1,9 @@
 """Parity of precog_scan_complex (Eq. 1 with the diagonal complex A of
 Sec. 3) with the fp64 oracle: full comparison of y and the complex hT at
-fp32 (bar 1e-5) on small shapes, the corpus-encode shape with bf16 inputs on
-sampled rows (bar 2e-3), and the exact reduction to the real scan when every
-frequency is zero."""
+fp32 (bar 1e-5) on small shapes, one pass and cut into time chunks (summary
+pass, complex carry fold, replay), the corpus-encode and long-context shapes
+with bf16 inputs on sampled rows (bar 2e-3), agreement across chunk lengths,
+and the exact reduction to the real scan when every frequency is zero."""
 import numpy as np
 import pytest
 import torch
@@ -49,7 +50,7 @@ def test_complex_scan_zero_frequency_equals_real_scan():
     h0r = torch.from_numpy(np.random.default_rng(3).normal(0, 0.5, (2, 256, 16))).float().to(DEV)
     h0c = torch.stack([h0r, torch.zeros_like(h0r)], dim=-1).contiguous()
     y_c, h_c = P.scan_complex(d["x"], d["dt"], d["A"], torch.zeros_like(d["A"]), d["B"], d["C"],
-                              d["z"], d["Dskip"], h0c)
+                              d["z"], d["Dskip"], h0c, chunk=300)
     y_r, h_r = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0r,
                       chunk=300)  # one pass, as the complex kernel
     torch.cuda.synchronize()
@@ -97,3 +98,102 @@ def test_complex_encode_workload_sampled():
                                            inp["Dskip"][dd:dd + 1].cpu())
         assert err_rms(y[b:b + 1, :, dd:dd + 1].double().cpu().numpy(), y_ref) <= TOL_BF16, (b, dd)
         assert err_rms(hT[b:b + 1, dd:dd + 1].double().cpu().numpy(), h_ref) <= TOL_BF16, (b, dd)
+
+
+@pytest.mark.parametrize("chunk", [16, 64, 100, 0])
+def test_complex_chunked_fp32(chunk):
+    """Cut into chunks of 16, 64 and 100 tokens (the last one ragged) and the
+    automatic choice, from a nonzero complex h0: the carried states decay by
+    exp(-a sum dt) ~ 0.1 over a 16-token chunk here, so the fold's magnitude
+    and rotation both reach the outputs.  Full comparison at fp32."""
+    B, L, D, N = 2, 1000, 128, 16
+    inp = synth.scan_inputs_host(B, L, D, N, seed=501, in_dtype=torch.float32)
+    A_im = synth.complex_frequencies(D, N)
+    h0 = torch.from_numpy(np.random.default_rng(502).normal(0, 0.5, (B, D, N, 2))).float()
+    d = _dev(inp)
+    y, hT = P.scan_complex(d["x"], d["dt"], d["A"], A_im.to(DEV), d["B"], d["C"], d["z"],
+                           d["Dskip"], h0.to(DEV), chunk=chunk)
+    torch.cuda.synchronize()
+    y_ref, h_ref = oracle.scan_complex(inp["x"], inp["dt"], inp["A"], A_im, inp["B"], inp["C"],
+                                       inp["z"], inp["Dskip"], h0)
+    ey = err_rms(y.double().cpu().numpy(), y_ref)
+    eh = err_rms(hT.double().cpu().numpy(), h_ref)
+    print("complex chunk=%d: err y %.3g hT %.3g" % (chunk, ey, eh))
+    assert ey <= TOL_F32 and eh <= TOL_F32
+
+
+def test_complex_chunked_state_only_and_h0_stride():
+    """State-only chunked scan with h0 and hT at a batch stride larger than
+    2 D N (rows of a wider store), fp16 states."""
+    B, L, D, N = 3, 600, 64, 8
+    inp = synth.scan_inputs_host(B, L, D, N, seed=503, in_dtype=torch.float32)
+    A_im = synth.complex_frequencies(D, N)
+    h0 = torch.from_numpy(np.random.default_rng(504).normal(0, 0.5, (B, D, N, 2)))
+    h0_16 = h0.to(torch.float16)
+    stride = 2 * D * N + 64
+    h0s = torch.zeros((B, stride), dtype=torch.float16)
+    h0s[:, :2 * D * N] = h0_16.reshape(B, -1)
+    hTs = torch.zeros((B, stride), dtype=torch.float16, device=DEV)
+    d = _dev(inp)
+    desc = P.scan_desc(B, L, D, N, P.F32, P.F32, P.F16, h0_batch_stride=stride,
+                       hT_batch_stride=stride, chunk=50)
+    nws = P.scan_complex_workspace_bytes(desc)
+    ws = torch.empty(nws, dtype=torch.uint8, device=DEV)
+    P.scan_complex_raw(desc, d["x"], d["dt"], d["A"], A_im.to(DEV), d["B"], None, None, None,
+                       h0s.to(DEV), None, hTs, ws, nws)
+    torch.cuda.synchronize()
+    _, h_ref = oracle.scan_complex(inp["x"], inp["dt"], inp["A"], A_im, inp["B"], None, None,
+                                   None, h0_16.float(), want_y=False)
+    got = hTs[:, :2 * D * N].reshape(B, D, N, 2).double().cpu().numpy()
+    assert err_rms(got, h_ref) <= TOL_BF16
+    assert not torch.any(hTs[:, 2 * D * N:])  # nothing written past each row
+
+
+def test_complex_chunked_zero_frequency_equals_real_chunked_scan():
+    """w = 0: the chunked complex scan performs the real chunked scan's fp32
+    operations (summary, fold with cos 0 = 1 and sin 0 = 0, replay), so with
+    the same chunks y and Re hT are bitwise equal and Im hT is zero."""
+    inp = synth.scan_inputs_host(2, 700, 256, 16, seed=505, in_dtype=torch.bfloat16)
+    d = _dev(inp)
+    h0r = torch.from_numpy(np.random.default_rng(506).normal(0, 0.5, (2, 256, 16))).float().to(DEV)
+    h0c = torch.stack([h0r, torch.zeros_like(h0r)], dim=-1).contiguous()
+    y_c, h_c = P.scan_complex(d["x"], d["dt"], d["A"], torch.zeros_like(d["A"]), d["B"], d["C"],
+                              d["z"], d["Dskip"], h0c, chunk=64)
+    y_r, h_r = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0r,
+                      chunk=64)
+    torch.cuda.synchronize()
+    assert torch.equal(y_c, y_r)
+    assert torch.equal(h_c[..., 0], h_r) and not torch.any(h_c[..., 1])
+
+
+def test_complex_long_context_sampled_and_chunk_sweep():
+    """The long-context shape (8 x 65,536 tokens, D=2048, N=16, bf16) with
+    w_n = pi n, in 256-token chunks and with the automatic chunking: sampled
+    rows against the oracle (y fp32, hT fp32), and the two chunkings agree."""
+    wl = synth.LONG_CONTEXT
+    B, L, D, N = wl.batch, wl.seqlen, wl.dim, wl.dstate
+    inp = synth.scan_inputs_device(B, L, D, N, wl.seed + 40, torch.bfloat16)
+    A_im = synth.complex_frequencies(D, N).to(DEV)
+    rows = sample_rows(B, D, 10, seed=41)
+    outs = {}
+    for chunk in (wl.chunk, 0):
+        y, hT = P.scan_complex(inp["x"], inp["dt"], inp["A"], A_im, inp["B"], inp["C"], inp["z"],
+                               inp["Dskip"], out_dtype=torch.float32, state_dtype=torch.float32,
+                               chunk=chunk)
+        torch.cuda.synchronize()
+        outs[chunk] = (torch.stack([y[b, :, dd] for b, dd in rows]).cpu(),
+                       torch.stack([hT[b, dd] for b, dd in rows]).cpu())
+        del y, hT
+    for i, (b, dd) in enumerate(rows):
+        sl = lambda t: t[b:b + 1, :, dd:dd + 1].cpu()
+        y_ref, h_ref = oracle.scan_complex(sl(inp["x"]), sl(inp["dt"]), inp["A"][dd:dd + 1].cpu(),
+                                           A_im[dd:dd + 1].cpu(), inp["B"][b:b + 1].cpu(),
+                                           inp["C"][b:b + 1].cpu(), sl(inp["z"]),
+                                           inp["Dskip"][dd:dd + 1].cpu())
+        for chunk, (ys, hs) in outs.items():
+            assert err_rms(ys[i].double().numpy(), y_ref[0, :, 0]) <= TOL_BF16, (chunk, b, dd)
+            assert err_rms(hs[i].double().numpy(), h_ref[0, 0]) <= TOL_BF16, (chunk, b, dd)
+    ya, ha = outs[wl.chunk]
+    yb, hb = outs[0]
+    assert err_rms(ya.double().numpy(), yb.double().numpy()) <= TOL_F32
+    assert err_rms(ha.double().numpy(), hb.double().numpy()) <= TOL_F32
