@@ -18,6 +18,9 @@ What each function follows in the paper (arXiv 2608.02560):
   (Sec. 5.2).
 * ``topk_compose``-- softmax-weighted composition of the top-k states
   (Sec. 5.4, Eq. smc-fusion; Fig. 1 caption).
+* ``fuse``        -- joint episodic + corpus retrieval: the k best candidates
+  of both stores composed, plus the session's semantic state as a baseline
+  term (Sec. 5.4, Eq. smc-fusion).
 * ``route2``, ``ema``, ``consolidate`` -- SMC two-stage routing (Sec. 5.1,
   Eqs. smc-domain, smc-sub) and semantic EMA consolidation (Sec. 5.3,
   Eq. smc-ema), one update and a chunk-ordered sequence of them.
@@ -206,6 +209,42 @@ def topk_compose(store, idx, scores, tau):
         tot = sum(w)
         for j in range(k):
             out[qi] += (w[j] / tot) * store[int(idx[qi, j])]
+    return out
+
+
+def fuse(episodic_store, episodic_idx, episodic_score, corpus_store, corpus_idx, corpus_score, k,
+         tau, semantic=None, semantic_row=None, lam=0.0):
+    """Joint retrieval at query time (Sec. 5.4, Eq. smc-fusion).  Per query
+    the candidates of the episodic store and of the corpus are ranked together
+    by score (larger first; equal scores: episodic before corpus, then the
+    lower row), the k best are composed with softmax(score / tau) weights,
+    and lam times the session's semantic state semantic[semantic_row[q]] is
+    added (nothing when semantic is None).  Candidates come as rows
+    [Q, k_e] / [Q, k_c] of each store with their scores.  Returns h_init
+    [Q, S] in fp64."""
+    ep = _f64(episodic_store)
+    co = _f64(corpus_store)
+    ei = np.asarray(episodic_idx, dtype=np.int64)
+    ci = np.asarray(corpus_idx, dtype=np.int64)
+    es = np.asarray(episodic_score, dtype=np.float64)
+    cs = np.asarray(corpus_score, dtype=np.float64)
+    Q = ei.shape[0]
+    S = ep.shape[1] if ep.ndim == 2 and ep.shape[0] > 0 else co.shape[1]
+    sem = _f64(semantic) if semantic is not None else None
+    out = np.zeros((Q, S))
+    for qi in range(Q):
+        cands = [(-float(es[qi, j]), 0, int(ei[qi, j])) for j in range(ei.shape[1])]
+        cands += [(-float(cs[qi, j]), 1, int(ci[qi, j])) for j in range(ci.shape[1])]
+        cands.sort()
+        top = cands[:k]
+        logits = [-c[0] / tau for c in top]
+        m = max(logits)
+        w = [np.exp(v - m) for v in logits]
+        tot = sum(w)
+        for (_, src, row), wj in zip(top, w):
+            out[qi] += (wj / tot) * (ep if src == 0 else co)[row]
+        if sem is not None:
+            out[qi] += lam * sem[int(semantic_row[qi])]
     return out
 
 

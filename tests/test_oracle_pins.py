@@ -377,6 +377,61 @@ def test_topk_compose_softmax_by_hand():
     assert np.allclose(out2[0], (1 - w1) * store[0].numpy() + w1 * store[1].numpy(), atol=1e-15)
 
 
+def test_fuse_by_hand():
+    """Episodic candidates: rows 0, 1 with scores log 3 and -10; corpus
+    candidates: rows 0, 1 with scores log 2 and 0.  The three best across
+    both stores are (log 3, episodic 0), (log 2, corpus 0), (0, corpus 1):
+    weights 3/6, 2/6, 1/6 at tau = 1.  With unit-vector states the fusion
+    is [1/2, 1/3, 1/6, 0]; the semantic state [0, 0, 0, 2] at weight 1/2
+    adds 1 in the last place."""
+    ep = torch.tensor([[1.0, 0.0, 0.0, 0.0], [0.0, 0.0, 0.0, 5.0]])
+    co = torch.tensor([[0.0, 1.0, 0.0, 0.0], [0.0, 0.0, 1.0, 0.0]])
+    ei, es = np.array([[0, 1]]), np.array([[np.log(3.0), -10.0]])
+    ci, cs = np.array([[0, 1]]), np.array([[np.log(2.0), 0.0]])
+    h = oracle.fuse(ep, ei, es, co, ci, cs, 3, 1.0)
+    assert np.allclose(h, [[0.5, 1 / 3, 1 / 6, 0.0]], rtol=0, atol=1e-15)
+    sem = torch.tensor([[9.0, 9.0, 9.0, 9.0], [0.0, 0.0, 0.0, 2.0]])
+    h2 = oracle.fuse(ep, ei, es, co, ci, cs, 3, 1.0, sem, np.array([1]), 0.5)
+    assert np.allclose(h2, [[0.5, 1 / 3, 1 / 6, 1.0]], rtol=0, atol=1e-15)
+    # k = 1: the single best candidate, weight 1; equal scores across the
+    # stores go to the episodic one
+    one = oracle.fuse(ep, ei, es, co, ci, cs, 1, 1.0)
+    assert np.array_equal(one, [[1.0, 0.0, 0.0, 0.0]])
+    tie = oracle.fuse(ep, np.array([[1]]), np.array([[0.25]]), co, np.array([[0]]),
+                      np.array([[0.25]]), 1, 1.0)
+    assert np.array_equal(tie, [[0.0, 0.0, 0.0, 5.0]])
+
+
+def test_fuse_equals_composition_over_the_joined_index():
+    """Fusing the two stores' top-k lists is the top-k composition over one
+    index holding the episodic keys then the corpus keys (its lower rows,
+    the episodic ones, win equal scores), with the states stacked the same
+    way; lam = 0 adds nothing and lam scales the semantic state linearly."""
+    g = np.random.default_rng(31)
+    Me, Mc, E, S, Q, k = 30, 50, 16, 24, 6, 4
+    qe, Ke, _, _ = synth.retrieval_inputs_host(Q, Me, E, 0, seed=32)
+    _, Kc, _, _ = synth.retrieval_inputs_host(1, Mc, E, 0, seed=33)
+    Kc[7] = Ke[3]  # a corpus key equal to an episodic one: equal scores
+    se = synth.state_store(Me, S, seed=34)
+    sc_ = synth.state_store(Mc, S, seed=35)
+    ie, ve = oracle.topk_scores(qe, Ke, k)
+    ic, vc = oracle.topk_scores(qe, Kc, k)
+    h = oracle.fuse(se, ie, ve, sc_, ic, vc, k, 0.7)
+    ij, vj = oracle.topk_scores(qe, torch.cat([Ke, Kc]), k)
+    ref = oracle.topk_compose(torch.cat([se, sc_]), ij, vj, 0.7)
+    assert np.allclose(h, ref, rtol=0, atol=1e-13)
+    sem = torch.from_numpy(g.normal(size=(5, S)))
+    rows = g.integers(0, 5, Q)
+    h0 = oracle.fuse(se, ie, ve, sc_, ic, vc, k, 0.7, sem, rows, 0.0)
+    h3 = oracle.fuse(se, ie, ve, sc_, ic, vc, k, 0.7, sem, rows, 3.0)
+    assert np.array_equal(h0, h)
+    assert np.allclose(h3 - h, 3.0 * sem.numpy()[rows], rtol=0, atol=1e-12)
+    # very sharp softmax: the single best candidate of either store
+    sharp = oracle.fuse(se, ie, ve, sc_, ic, vc, k, 1e-9)
+    best = oracle.gather(torch.cat([se, sc_]), ij[:, 0])
+    assert np.allclose(sharp, best, rtol=0, atol=1e-12)
+
+
 def test_route2_matches_numpy():
     g = np.random.default_rng(8)
     E = 24
