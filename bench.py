@@ -593,6 +593,40 @@ def bench_extensions(args, flush):
         P.scan_encode_indexed(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
                               inp["Dskip"], store3, M, idxk, y, hT, h0_score=sck, k=kk, tau=1.0)
 
+    # joint retrieval (Sec. 5.4): top-3 from a 500-entry episodic store and
+    # from the corpus, fused with the session's semantic state, then the
+    # prefill from the fused state
+    Me = 500
+    _, Ke, _, _ = synth.retrieval_inputs_host(1, Me, E, 0, cfg["seed"] + 1)
+    Ke = Ke.cuda()
+    se = synth.state_store(Me, D * N, seed=35, device="cuda")
+    sem = synth.state_store(20, D * N, seed=36, device="cuda")
+    srow = torch.arange(Q, dtype=torch.int32, device="cuda") % 20
+    nwe = P.retrieve_workspace_bytes(Q, Me, E)
+    wse = torch.empty(nwe, dtype=torch.uint8, device="cuda")
+    ie = torch.empty((Q, kk), dtype=torch.int32, device="cuda")
+    ve = torch.empty((Q, kk), dtype=torch.float64, device="cuda")
+    P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
+    P.retrieve_topk(q, Ke, kk, ie, ve, wse, nwe)
+    fuse = lambda: P.inject_fuse(se, ie, ve, store, idxk, sck, kk, 1.0, h0.view(Q, -1), sem, srow,
+                                 1.0)
+    fu_ms = time_events(fuse, 20, flush, hold=True)
+
+    def joint():
+        P.retrieve_topk(q, Ke, kk, ie, ve, wse, nwe)
+        P.retrieve_topk(q, K, kk, idxk, sck, ws, nws)
+        fuse()
+        P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
+                      inp["Dskip"], h0, y, hT)
+
+    res["joint_query_path"] = {
+        "workload": "256 queries: top-3 over a 500-entry episodic store and over the corpus "
+                    "(10,000 keys), fused with the session's semantic state (lambda = 1), "
+                    "32-token bf16 prefill from the fused state; cold cache, GPU time",
+        "fuse_us": fu_ms * 1e3,
+        "fuse_gbps": (2 * kk + 2) * Q * D * N * 2 / (fu_ms * 1e-3) / 1e9,
+        "end_to_end_us": time_events(joint, 20, flush, hold=True) * 1e3}
+    del se, sem, wse, Ke
     res["query_path_top3"] = {
         "workload": "the query path with top-3 retrieval and softmax composition (tau = 1), "
                     "cold cache, GPU time",

@@ -26,6 +26,8 @@
  *                           the same retrieval over an index prepared once
  *   precog_inject_compose   softmax-weighted composition of the top-k states
  *                           (Sec. 5.4 Eq. smc-fusion)
+ *   precog_inject_fuse      the same over an episodic and a corpus store, plus
+ *                           the session's semantic state (Sec. 5.4)
  * and the memory-consolidation steps of SMC:
  *   precog_smc_route        two-stage cluster routing (Sec. 5.1)
  *   precog_smc_consolidate  semantic-state EMA (Sec. 5.3 Eq. smc-ema)
@@ -382,6 +384,48 @@ precog_status precog_inject_compose(const void *state_store,
 /* ------------------------------------------------------------------------ */
 /* Structured Memory Consolidation (Sec. 5)                                 */
 /* ------------------------------------------------------------------------ */
+
+/* Joint retrieval at query time (Sec. 5.4, Eq. smc-fusion): the candidates
+ * of the session's episodic store and of the corpus, each from its own exact
+ * top-k (precog_retrieve_topk over its own key index with the same query
+ * embedding), are ranked together by score -- larger first; equal scores:
+ * episodic before corpus, then the lower row, then the earlier list entry --
+ * and the k best are composed as in precog_inject_compose, plus the
+ * session's semantic state s with weight lambda (the paper adds it as a
+ * baseline term and gives no weight; lambda = 1 adds it as is, 0 leaves it
+ * out):
+ *   h0[q] = sum_{j<k} w_j h^(j) + lambda * semantic[semantic_row[q]],
+ *   w = softmax(score / tau) over the k selected scores.
+ *   episodic_store [episodic_rows, S], corpus_store [corpus_rows, S] and
+ *              semantic [semantic_rows, S]: store_dtype (F32 | F16)
+ *   episodic_idx / episodic_score  [Q, episodic_k] int32 / fp64
+ *   corpus_idx / corpus_score      [Q, corpus_k] int32 / fp64
+ *              (episodic_k, corpus_k in 0..64; either list may be empty)
+ *   k          1..64, k <= episodic_k + corpus_k
+ *   semantic   NULL: no baseline term (semantic_row, lambda unread);
+ *              semantic_row [Q] int32, e.g. the flat sub-cluster that
+ *              precog_smc_route returned for the session
+ *   h0         [Q, S] output in h0_dtype (F32 | F16, RNE)
+ *   S % 8 == 0; tau > 0 finite; lambda finite; pointers 16-byte aligned.
+ * Arithmetic: the weights as precog_inject_compose forms them (fp64, rounded
+ * once to fp32), then one fp32 fma per term in rank order and one for the
+ * semantic term.  With an empty corpus list and no semantic state the result
+ * equals precog_inject_compose's bit for bit.  A candidate or semantic row
+ * outside its store gives a NaN row. */
+precog_status precog_inject_fuse(const void *episodic_store,
+                                 int64_t episodic_rows,
+                                 const int32_t *episodic_idx,
+                                 const double *episodic_score,
+                                 int64_t episodic_k, const void *corpus_store,
+                                 int64_t corpus_rows,
+                                 const int32_t *corpus_idx,
+                                 const double *corpus_score, int64_t corpus_k,
+                                 precog_dtype store_dtype, int64_t S, int64_t Q,
+                                 int64_t k, double tau, const void *semantic,
+                                 const int32_t *semantic_row,
+                                 int64_t semantic_rows, double lambda,
+                                 void *h0, precog_dtype h0_dtype,
+                                 void *stream);
 
 /* Two-stage routing of Sec. 5.1 (Eqs. smc-domain, smc-sub) for C chunk
  * embeddings phi(c):

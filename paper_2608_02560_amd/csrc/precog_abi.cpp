@@ -539,6 +539,71 @@ precog_status precog_inject_compose(const void* state_store, precog_dtype store_
   return PRECOG_OK;
 }
 
+precog_status precog_inject_fuse(const void* episodic_store, int64_t episodic_rows,
+                                 const int32_t* episodic_idx, const double* episodic_score,
+                                 int64_t episodic_k, const void* corpus_store, int64_t corpus_rows,
+                                 const int32_t* corpus_idx, const double* corpus_score,
+                                 int64_t corpus_k, precog_dtype store_dtype, int64_t S, int64_t Q,
+                                 int64_t k, double tau, const void* semantic,
+                                 const int32_t* semantic_row, int64_t semantic_rows,
+                                 double lambda, void* h0, precog_dtype h0_dtype, void* stream) {
+  if (episodic_rows < 0 || corpus_rows < 0 || S < 0 || Q < 0 || semantic_rows < 0)
+    return PRECOG_ERR_SHAPE;
+  if (episodic_k < 0 || episodic_k > precog::kMaxTopK || corpus_k < 0 ||
+      corpus_k > precog::kMaxTopK || k < 1 || k > precog::kMaxTopK ||
+      k > episodic_k + corpus_k)
+    return PRECOG_ERR_SHAPE;
+  if (!(tau > 0.0) || !std::isfinite(tau) || !std::isfinite(lambda)) return PRECOG_ERR_SHAPE;
+  if ((store_dtype != PRECOG_F32 && store_dtype != PRECOG_F16) ||
+      (h0_dtype != PRECOG_F32 && h0_dtype != PRECOG_F16))
+    return PRECOG_ERR_DTYPE;
+  if (S % 8 != 0) return PRECOG_ERR_ALIGN;
+  if (Q == 0 || S == 0) return PRECOG_OK;
+  if (!h0) return PRECOG_ERR_NULL;
+  if (episodic_k > 0 && (!episodic_idx || !episodic_score || (episodic_rows > 0 && !episodic_store)))
+    return PRECOG_ERR_NULL;
+  if (corpus_k > 0 && (!corpus_idx || !corpus_score || (corpus_rows > 0 && !corpus_store)))
+    return PRECOG_ERR_NULL;
+  if (semantic && !semantic_row) return PRECOG_ERR_NULL;
+  const void* ptrs[] = {episodic_store, episodic_idx, episodic_score, corpus_store, corpus_idx,
+                        corpus_score, semantic, semantic_row, h0};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
+  if (S / 8 / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  const precog_status st = check_device();
+  if (st != PRECOG_OK) return st;
+
+  (void)hipGetLastError();
+  const int out_bytes = h0_dtype == PRECOG_F32 ? 4 : 2;
+  // gridDim.y is limited to 65535: walk the queries in slices
+  for (int64_t q0 = 0; q0 < Q; q0 += 65535) {
+    precog::FuseParams p{};
+    p.store[0] = episodic_store;
+    p.store[1] = corpus_store;
+    p.rows[0] = episodic_rows;
+    p.rows[1] = corpus_rows;
+    p.idx[0] = episodic_k ? episodic_idx + q0 * episodic_k : nullptr;
+    p.idx[1] = corpus_k ? corpus_idx + q0 * corpus_k : nullptr;
+    p.score[0] = episodic_k ? episodic_score + q0 * episodic_k : nullptr;
+    p.score[1] = corpus_k ? corpus_score + q0 * corpus_k : nullptr;
+    p.kk[0] = static_cast<int>(episodic_k);
+    p.kk[1] = static_cast<int>(corpus_k);
+    p.sem = semantic;
+    p.sem_row = semantic ? semantic_row + q0 : nullptr;
+    p.sem_rows = semantic_rows;
+    p.lambda = static_cast<float>(lambda);
+    p.out = static_cast<char*>(h0) + q0 * S * out_bytes;
+    p.S = S;
+    p.Q = (Q - q0) < 65535 ? (Q - q0) : 65535;
+    p.k = static_cast<int>(k);
+    p.inv_tau = 1.0 / tau;
+    const hipError_t e = precog::launch_fuse(p, store_dtype, h0_dtype,
+                                             static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return PRECOG_ERR_HIP;
+  }
+  return PRECOG_OK;
+}
+
 precog_status precog_smc_route(const float* emb, int64_t C, int64_t E, const float* domain_protos,
                               int64_t n_domains, const float* sub_protos, int64_t n_sub,
                               int32_t* domain_out, int32_t* sub_out, int32_t* flat_out,

@@ -122,6 +122,23 @@ struct ComposeParams {
 hipError_t launch_compose(const ComposeParams& p, int store_dtype, int out_dtype,
                           hipStream_t s);
 
+struct FuseParams {
+  const void* store[2];     // episodic [rows[0], S] and corpus [rows[1], S] states
+  int64_t rows[2];
+  const int32_t* idx[2];    // [Q, kk[s]] candidate rows of store s
+  const double* score[2];   // [Q, kk[s]] their scores
+  int kk[2];                // candidates per query in each list, 0..kMaxTopK
+  const void* sem;          // [sem_rows, S] semantic states, or null
+  const int32_t* sem_row;   // [Q] row of the session's semantic state
+  int64_t sem_rows;
+  float lambda;             // weight of the semantic state
+  void* out;                // [Q, S]
+  int64_t S, Q;
+  int k;                    // candidates composed, 1..kMaxTopK
+  double inv_tau;           // 1 / temperature
+};
+hipError_t launch_fuse(const FuseParams& p, int store_dtype, int out_dtype, hipStream_t s);
+
 struct RouteParams {
   const float* emb;    // [C, E] chunk embeddings
   const float* dom;    // [ndom, E] domain prototypes

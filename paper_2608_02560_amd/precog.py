@@ -31,6 +31,7 @@ EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_enc
            "precog_retrieve_top1_noalloc",
            "precog_retrieve_topk", "precog_retrieve_index_bytes", "precog_retrieve_prepare",
            "precog_retrieve_topk_prepared", "precog_inject_gather", "precog_inject_compose",
+           "precog_inject_fuse",
            "precog_smc_route", "precog_smc_consolidate", "precog_status_string")
 
 
@@ -97,6 +98,10 @@ def lib():
         L.precog_inject_compose.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, i64, i64,
                                             ctypes.c_double, vp, ctypes.c_int, vp]
         L.precog_inject_compose.restype = ctypes.c_int
+        L.precog_inject_fuse.argtypes = [vp, i64, vp, vp, i64, vp, i64, vp, vp, i64, ctypes.c_int,
+                                         i64, i64, i64, ctypes.c_double, vp, vp, i64,
+                                         ctypes.c_double, vp, ctypes.c_int, vp]
+        L.precog_inject_fuse.restype = ctypes.c_int
         L.precog_smc_route.argtypes = [vp, i64, i64, vp, i64, vp, i64, vp, vp, vp, vp]
         L.precog_smc_route.restype = ctypes.c_int
         L.precog_smc_consolidate.argtypes = [vp, ctypes.c_int, i64, i64, vp, ctypes.c_int, vp, i64,
@@ -268,6 +273,25 @@ def inject_gather(store, idx, h0, stream=None):
     st = lib().precog_inject_gather(_ptr(store), _DT[store.dtype], M, S, _ptr(idx),
                                     idx.shape[0], _ptr(h0), _DT[h0.dtype], _stream(stream))
     _check("precog_inject_gather", st)
+
+
+def inject_fuse(episodic_store, episodic_idx, episodic_score, corpus_store, corpus_idx,
+                corpus_score, k, tau, h0, semantic=None, semantic_row=None, lam=1.0,
+                stream=None):
+    """precog_inject_fuse: stores [M, ...] (same dtype), candidate lists
+    [Q, k_e] / [Q, k_c] (int32 rows, fp64 scores), h0 [Q, ...]."""
+    Q = h0.shape[0]
+    S = h0[0].numel() if Q > 0 else 0
+    ke = episodic_idx.shape[1] if episodic_idx is not None else 0
+    kc = corpus_idx.shape[1] if corpus_idx is not None else 0
+    st = lib().precog_inject_fuse(_ptr(episodic_store), episodic_store.shape[0],
+                                  _ptr(episodic_idx), _ptr(episodic_score), ke,
+                                  _ptr(corpus_store), corpus_store.shape[0], _ptr(corpus_idx),
+                                  _ptr(corpus_score), kc, _DT[episodic_store.dtype], S, Q, int(k),
+                                  float(tau), _ptr(semantic), _ptr(semantic_row),
+                                  semantic.shape[0] if semantic is not None else 0, float(lam),
+                                  _ptr(h0), _DT[h0.dtype], _stream(stream))
+    _check("precog_inject_fuse", st)
 
 
 def smc_route(emb, domain_protos, sub_protos, domain_out, sub_out, flat_out=None, stream=None):

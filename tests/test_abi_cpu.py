@@ -280,6 +280,37 @@ def test_compose_validation_errors():
     assert call(Q=0) == OK
 
 
+def test_fuse_validation_errors():
+    L = P.lib()
+
+    def call(es=FAKE, er=10, ei=FAKE, esc=FAKE, ek=3, cs=FAKE, cr=20, ci=FAKE, csc=FAKE, ck=3,
+             sd=P.F16, S=64, Q=3, k=3, tau=1.0, sem=None, srow=None, sr=0, lam=1.0, h=FAKE,
+             hd=P.F32):
+        return L.precog_inject_fuse(es, er, ei, esc, ek, cs, cr, ci, csc, ck, sd, S, Q, k, tau, sem,
+                                    srow, sr, lam, h, hd, None)
+    assert call(k=0) == ESHAPE
+    assert call(k=7) == ESHAPE                 # more than the two lists hold
+    assert call(ek=65) == ESHAPE
+    assert call(ck=-1) == ESHAPE
+    assert call(er=-1) == ESHAPE
+    assert call(tau=0.0) == ESHAPE
+    assert call(tau=float("inf")) == ESHAPE
+    assert call(lam=float("nan")) == ESHAPE
+    assert call(sd=P.BF16) == EDTYPE
+    assert call(hd=P.BF16) == EDTYPE
+    assert call(S=12) == EALIGN
+    assert call(ei=None) == ENULL
+    assert call(csc=None) == ENULL
+    assert call(cs=None) == ENULL
+    assert call(sem=FAKE, srow=None, sr=4) == ENULL
+    assert call(h=None) == ENULL
+    assert call(esc=FAKE + 8) == EALIGN
+    assert call(srow=FAKE + 4, sem=FAKE, sr=4) == EALIGN
+    assert call(Q=0) == OK
+    # an empty list needs none of its pointers
+    assert call(ck=0, ci=None, csc=None, cs=None, Q=0) == OK
+
+
 def test_smc_validation_errors():
     L = P.lib()
     route = lambda e=FAKE, C=3, E=16, d=FAKE, nd=5, s=FAKE, ns=4, mo=FAKE, so=FAKE, fo=None: \
