@@ -127,16 +127,21 @@ precog_status validate_desc(const precog_scan_desc* d) {
 extern "C" {
 
 const char* precog_status_string(precog_status s) {
-  switch (s) {
-    case PRECOG_OK: return "ok";
-    case PRECOG_ERR_NULL: return "a required pointer is NULL";
-    case PRECOG_ERR_SHAPE: return "unsupported or negative size";
-    case PRECOG_ERR_DTYPE: return "unsupported dtype for this tensor";
-    case PRECOG_ERR_STRIDE: return "state batch stride smaller than D*N";
-    case PRECOG_ERR_ALIGN: return "pointer or size breaks the alignment rule";
-    case PRECOG_ERR_WORKSPACE: return "workspace missing or too small";
-    case PRECOG_ERR_ARCH: return "current device is not gfx950";
-    case PRECOG_ERR_HIP: return "HIP runtime call or launch failed";
+  // A C caller may pass any int: read the code as one, since loading an
+  // enum object that holds a value outside the enum's range is undefined in
+  // C++.
+  int code = 0;
+  std::memcpy(&code, &s, sizeof code);
+  switch (code) {
+    case static_cast<int>(PRECOG_OK): return "ok";
+    case static_cast<int>(PRECOG_ERR_NULL): return "a required pointer is NULL";
+    case static_cast<int>(PRECOG_ERR_SHAPE): return "unsupported or negative size";
+    case static_cast<int>(PRECOG_ERR_DTYPE): return "unsupported dtype for this tensor";
+    case static_cast<int>(PRECOG_ERR_STRIDE): return "state batch stride smaller than D*N";
+    case static_cast<int>(PRECOG_ERR_ALIGN): return "pointer or size breaks the alignment rule";
+    case static_cast<int>(PRECOG_ERR_WORKSPACE): return "workspace missing or too small";
+    case static_cast<int>(PRECOG_ERR_ARCH): return "current device is not gfx950";
+    case static_cast<int>(PRECOG_ERR_HIP): return "HIP runtime call or launch failed";
   }
   return "unknown status";
 }
