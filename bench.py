@@ -21,7 +21,8 @@ timed beside it on the host cores:
 
 and the extensions (top-k composition, SMC trajectory / routing /
 consolidation, complex-A scan) under "extensions".  --quick times the
-headline alone.
+headline alone; --only NAME times one of the others alone (for profiling) and
+prints its figures instead of the headline line.
 """
 from __future__ import annotations
 
@@ -726,6 +727,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip every oracle timing")
     ap.add_argument("--quick", action="store_true", help="time the headline workload only")
+    ap.add_argument("--only", choices=("single_layer", "query_path", "long_context", "large_corpus",
+                                       "extensions"),
+                    help="time one other workload alone and print its figures (for profiling); "
+                         "no headline line")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (traffic-counter calibration)")
     args = ap.parse_args()
@@ -746,6 +751,15 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n,
                           "launches": 3}), flush=True)
+        return
+    if args.only:
+        buf, flush = make_flush()
+        run = {"single_layer": lambda: bench_single_layer(args, flush),
+               "query_path": lambda: bench_query_path(args, flush),
+               "long_context": lambda: bench_long_context(args),
+               "large_corpus": lambda: bench_large_corpus(args),
+               "extensions": lambda: bench_extensions(args, flush)}[args.only]
+        print(json.dumps({"only": args.only, args.only: run()}), flush=True)
         return
     t_start = time.perf_counter()
     out, cpu = bench_corpus(args)
