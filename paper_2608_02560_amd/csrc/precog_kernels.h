@@ -85,6 +85,8 @@ struct RetrieveParams {
   int nqg;             // 32-query groups, padded to whole screen workgroups
   int nks;             // ceil(E / 16): 16-feature steps
   int k;               // keys kept per query, 1..kMaxTopK
+  // error-bound constants of the decide (set by launch_retrieve from E)
+  double err_g, err_h, err_tiny, err_gs;
 };
 // Screen workgroup: kRetWaves waves of 32 queries each, over kRetBlocks
 // blocks of 32 keys.

@@ -9,7 +9,7 @@
 //            components clear of the fp16 subnormal range) and stores the
 //            values in the order the matrix-core operands are consumed, so a
 //            wave's operand load is one contiguous 1 KiB segment.
-//   screen   workgroup = 64 keys x 128 queries: the keys are read
+//   screen   workgroup = 64 keys x 256 queries: the keys are read
 //            row-contiguously, rounded the same way and staged in LDS; each
 //            wave computes 32 queries against them with
 //            v_mfma_f32_32x32x16_f16 (each product of two fp16 values is
@@ -33,6 +33,8 @@
 //            the result is exact.  A query or key of norm 245 or more could
 //            leave the fp16 range (2^8 |v| past 65504); then the screen
 //            proves nothing and every key is scored in fp64.
+#include <cmath>
+
 #include "precog_kernels.h"
 #include "wave_ops.h"
 
@@ -500,30 +502,11 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   nmax = wave_max(nmax);
   const float tk = found ? tv : -INFINITY;
 
-  // Screen-score error bound.  Each operand value w = fp16(2^8 v) / 2^8
-  // has |w - v| <= a |v| + bs: a = 2^-11 (round to nearest in the fp16
-  // normal range), bs = 2^-22 (below it, whether rounded to a subnormal or
-  // flushed to zero).  So |q~ k~ - q k| <= (2a + a^2) |q k| + bs (1 + a)
-  // (|q| + |k|) + bs^2 per feature; summed with Cauchy-Schwarz for the
-  // products and |v|_1 <= sqrt(E) |v| for the 1-norms.  The fp32 sum of the E
-  // exact products adds at most 2 gamma_E times their absolute sum (twice
-  // the round-to-nearest bound, so additions that truncate, or align the
-  // products of one instruction to the largest, are covered too); the 2^-16
-  // scale back is exact (or below 2^-149).  The factor 1.01 covers the fp32
-  // norms (relative error ~gamma_E) and 1e-12 the fp64 reference's own
-  // rounding.  A norm past kMaxNorm2 could overflow fp16 (2^8 |v| >= 65520):
-  // then every key is scored exactly.
-  const double u = 5.9604644775390625e-08;  // 2^-24
-  const double a = 4.8828125e-04;           // 2^-11
-  const double bs = 2.384185791015625e-07;  // 2^-22
-  const double en = static_cast<double>(E);
-  const double gam2 = 2.0 * (en * u) / (1.0 - en * u);
-  const double g = 1.01 * (2.0 * a + a * a + gam2 * (1.0 + 2.0 * a + a * a)) + 1e-12;
-  const double h = 1.01 * (1.0 + gam2) * bs * (1.0 + a) * sqrt(en);
-  const double tiny = 1.01 * (1.0 + gam2) * en * bs * bs + 1e-30;
+  // Screen-score error bound e(i) = g |q| |k_i| + h (|q| + |k_i|) + tiny;
+  // g, h and tiny depend on E only (error_bound_constants, on the host)
   const double qn = static_cast<double>(qnorm);
-  const double gq = g * qn + h;
-  const double hq = h * qn + tiny;
+  const double gq = p.err_g * qn + p.err_h;
+  const double hq = p.err_h * qn + p.err_tiny;
   // error bound of a screen score whose key has squared norm <= n2
   auto err = [&](float n2) { return gq * sqrt(static_cast<double>(n2)) + hq; };
   const bool exhaustive = !(qnorm2 < kMaxNorm2) || !(nmax < kMaxNorm2);
@@ -761,9 +744,7 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
       li = cand[0];
       done = true;
     } else {
-      const double u53 = 1.1102230246251565e-16;  // 2^-53
-      const double nf = static_cast<double>(E / 64 + 7);
-      const double gs = 1.01 * (nf * u53 / (1.0 - nf * u53) + en * u53 / (1.0 - en * u53));
+      const double gs = p.err_gs;
       double best = 0.0, best_mu = 0.0, others = -INFINITY;
       int best_i = -1;
       for (int c0 = 0; c0 < ncand; c0 += batch_max) {
@@ -802,7 +783,42 @@ __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
 
 }  // namespace
 
-hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s) {
+// The constants of the decide's error bounds, from E alone.
+// Screen scores: each operand value w = fp16(2^8 v) / 2^8 has |w - v| <=
+// a |v| + bs with a = 2^-11 (round to nearest in the fp16 normal range) and
+// bs = 2^-22 (below it, whether rounded to a subnormal or flushed to zero).
+// So |q~ k~ - q k| <= (2a + a^2) |q k| + bs (1 + a) (|q| + |k|) + bs^2 per
+// feature; summed with Cauchy-Schwarz for the products and |v|_1 <= sqrt(E)
+// |v| for the 1-norms.  The fp32 sum of the E exact products adds at most
+// 2 gamma_E times their absolute sum (twice the round-to-nearest bound, so
+// additions that truncate, or align the products of one instruction to the
+// largest, are covered too); the 2^-16 scale back is exact (or below
+// 2^-149).  The factor 1.01 covers the fp32 norms (relative error
+// ~gamma_E) and 1e-12 the fp64 reference's own rounding.  A norm past
+// kMaxNorm2 could overflow fp16 (2^8 |v| >= 65520): then every key is
+// scored exactly.
+// Lane-parallel fp64 sums (top-1 fast ordering): a sum of E / 64 features
+// per lane followed by a 6-level tree is within gamma_{E/64+7} sum |p_e| of
+// the exact sum, the sequential sum of the definition within gamma_E
+// sum |p_e|; err_gs bounds both together per unit of |q| |k| (1.01 for the
+// fp32 norms).
+static void error_bound_constants(RetrieveParams& p) {
+  const double u = 5.9604644775390625e-08;  // 2^-24
+  const double a = 4.8828125e-04;           // 2^-11
+  const double bs = 2.384185791015625e-07;  // 2^-22
+  const double en = static_cast<double>(p.E);
+  const double gam2 = 2.0 * (en * u) / (1.0 - en * u);
+  p.err_g = 1.01 * (2.0 * a + a * a + gam2 * (1.0 + 2.0 * a + a * a)) + 1e-12;
+  p.err_h = 1.01 * (1.0 + gam2) * bs * (1.0 + a) * std::sqrt(en);
+  p.err_tiny = 1.01 * (1.0 + gam2) * en * bs * bs + 1e-30;
+  const double u53 = 1.1102230246251565e-16;  // 2^-53
+  const double nf = static_cast<double>(p.E / 64 + 7);
+  p.err_gs = 1.01 * (nf * u53 / (1.0 - nf * u53) + en * u53 / (1.0 - en * u53));
+}
+
+hipError_t launch_retrieve(const RetrieveParams& pin, hipStream_t s) {
+  RetrieveParams p = pin;
+  error_bound_constants(p);
   if (p.nkb > 0) {
     const int64_t entries = static_cast<int64_t>(p.nqg) * p.nks * 64;
     hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, s, p);
