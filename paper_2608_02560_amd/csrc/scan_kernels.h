@@ -495,16 +495,6 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   const uint32_t el =
       static_cast<uint32_t>(16 * grp + (lane16 < NL ? lane16 : NL - 1)) * sizeof(TIn);
 
-  // Software pipeline over tiles of kPF tokens with two register buffers:
-  // while tile i is computed from one buffer, tile i + 1 streams into the
-  // other.  Each buffer keeps fixed registers (no rotation), and a buffer is
-  // refilled only after its tile has been consumed.  Tiles past the chunk
-  // reread its last token (in bounds, never used), so loads need no guards.
-  struct Tile {
-    typename SI::raw x[kPF], dt[kPF], z[kPF], b[kPF][G], c[kPF][G];
-  };
-  Tile t0b, t1b;
-
   // With 16 states per lane, B_t / C_t of a tile are written (as fp32) to a
   // wave-private LDS slice when the tile is consumed, by the lanes that
   // loaded them, and each token reads its 16 (+16) coefficients back with
@@ -516,6 +506,27 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // readout-free N = 16 scan saves only the 16 B broadcasts, less than the
   // staging costs.
   constexpr bool kLds = NL == 16 && (kRead || P > 1);
+  // 16-bit coefficients with N = 16 in one lane: a 4-token tile's B (and C)
+  // rows are 4 x 16 x 2 bytes = 32 dwords, so lanes 0..31 fetch one dword
+  // each (token l / 8, coefficients 2 (l mod 8) and 2 (l mod 8) + 1): one
+  // load per array and tile instead of one per token, and two 16-bit LDS
+  // writes (low half, high half) per lane (2.5% on the corpus encode,
+  // 3.5% on the query prefill).
+  constexpr bool kBcWord = kLds && P == 1 && sizeof(typename SI::raw) == 2 && kPF == 4;
+
+  // Software pipeline over tiles of kPF tokens with two register buffers:
+  // while tile i is computed from one buffer, tile i + 1 streams into the
+  // other.  Each buffer keeps fixed registers (no rotation), and a buffer is
+  // refilled only after its tile has been consumed.  Tiles past the chunk
+  // reread its last token (in bounds, never used), so loads need no guards;
+  // the coefficient dwords of tokens past the chunk lie past the
+  // descriptor's range and read as zero (never used either).
+  struct Tile {
+    typename SI::raw x[kPF], dt[kPF], z[kPF], b[kPF][G], c[kPF][G];
+    uint32_t bw, cw;  // kBcWord: this lane's dword of the tile's B / C rows
+  };
+  Tile t0b, t1b;
+
   __shared__ __attribute__((aligned(16))) float bc_lds[kLds ? kSBlock / 64 : 1][kLds ? kPF : 1][2][kLds ? N : 1];
   // bf16 coefficients go in as raw bits into the high half of a word whose
   // low half is zero (cleared once, below): the word is then the exact fp32
@@ -535,7 +546,22 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     for (int i = lane; i < kPF * 2 * N; i += 64) slice[i] = 0.f;
   }
   auto stage = [&](const Tile& tb) {
-    if constexpr (kLds) {
+    if constexpr (kBcWord) {
+      if (lane < 32) {
+        // the dword's low half is coefficient j, its high half j + 1
+        const int k = lane >> 3;
+        const int j = 2 * (lane & 7);
+        const uint16_t b0 = static_cast<uint16_t>(tb.bw), b1 = static_cast<uint16_t>(tb.bw >> 16);
+        put(&bc_lds[wave][k][0][j], b0);
+        put(&bc_lds[wave][k][0][j + 1], b1);
+        if constexpr (kRead) {
+          const uint16_t c0 = static_cast<uint16_t>(tb.cw), c1 = static_cast<uint16_t>(tb.cw >> 16);
+          put(&bc_lds[wave][k][1][j], c0);
+          put(&bc_lds[wave][k][1][j + 1], c1);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the writes are done before any read
+    } else if constexpr (kLds) {
       if ((lane >> 4) < P) {
 #pragma unroll
         for (int k = 0; k < kPF; ++k) {
@@ -550,7 +576,16 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     }
   };
   const int last = nsteps > 0 ? nsteps - 1 : 0;
+  // lane offset of the coefficient dwords (lanes past 31 fetch nothing)
+  const uint32_t bcw_off =
+      lane < 32 ? static_cast<uint32_t>(lane >> 3) * bc_row + 4u * static_cast<uint32_t>(lane & 7)
+                : kDropOffset;
   auto fetch = [&](Tile& tb, int tile) {
+    if constexpr (kBcWord) {
+      const uint32_t sb = static_cast<uint32_t>(tile * kPF) * bc_row;
+      tb.bw = __builtin_amdgcn_raw_buffer_load_b32(rb, bcw_off, sb, 0);
+      if constexpr (kRead) tb.cw = __builtin_amdgcn_raw_buffer_load_b32(rc, bcw_off, sb, 0);
+    }
 #pragma unroll
     for (int k = 0; k < kPF; ++k) {
       int st = tile * kPF + k;
@@ -559,11 +594,13 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       tb.x[k] = SI::load(rx, dl, so);
       tb.dt[k] = SI::load(rd, dl, so);
       if constexpr (HASZ) tb.z[k] = SI::load(rz, dl, so);
-      const uint32_t sb = static_cast<uint32_t>(st) * bc_row;
+      if constexpr (!kBcWord) {
+        const uint32_t sb = static_cast<uint32_t>(st) * bc_row;
 #pragma unroll
-      for (int j = 0; j < G; ++j) {
-        tb.b[k][j] = SI::load(rb, el + 16 * j * sizeof(TIn), sb);
-        if constexpr (kRead) tb.c[k][j] = SI::load(rc, el + 16 * j * sizeof(TIn), sb);
+        for (int j = 0; j < G; ++j) {
+          tb.b[k][j] = SI::load(rb, el + 16 * j * sizeof(TIn), sb);
+          if constexpr (kRead) tb.c[k][j] = SI::load(rc, el + 16 * j * sizeof(TIn), sb);
+        }
       }
     }
   };
