@@ -55,7 +55,6 @@ constexpr int kKB = 32;       // keys per block (one MFMA tile's rows; block sum
 // (kFC / 16 x 4 VGPRs)
 constexpr int kFC = 128;
 constexpr int kKS = kFC / 16; // 16-feature MFMA steps per chunk
-constexpr int kRound = 1;     // chunks whose loads the screen issues together
 
 __device__ __forceinline__ float xor_shfl(float v, int m) {
   const int src = (static_cast<int>(threadIdx.x & 63) ^ m) * 4;
@@ -97,8 +96,10 @@ __global__ __launch_bounds__(256) void prep_kernel(const RetrieveParams p) {
 // Per 128-feature chunk the workgroup stages its blocks' key rows in LDS,
 // rounded to fp16(2^8 k) and laid out in operand order [kb][ks][h][row],
 // the row XOR-swizzled with (2 ks + h) so the staging writes and the operand
-// reads hit distinct banks; every wave loads its own query operands; all of
-// a chunk's loads are issued before the first wait.  MFMA operands: keys are
+// reads hit distinct banks; every wave loads its own query operands.  The
+// loads of chunk c + 1 are issued before chunk c is staged (two register
+// buffers, two LDS tiles), so a chunk's memory round trip overlaps the
+// previous chunk's staging and matrix work.  MFMA operands: keys are
 // the rows (A), queries the columns (B); lane l supplies row / column
 // l mod 32 and the 8 features of half h = l / 32 of the 16-feature step, so
 // each dot product is the same whatever order the instruction consumes
@@ -137,12 +138,8 @@ __global__ __launch_bounds__(64 * kRetWaves) void screen_kernel(const RetrievePa
   // loads stay in bounds and whose results are discarded)
   const int64_t g = active ? qw / 32 : p.nqg - 1;
 
-  // A round covers kRound chunks of kFC features: every load of the round
-  // is issued before the first wait, so a workgroup pays one memory latency
-  // per round (one for E <= kRound kFC), each chunk staged in its own LDS
-  // tile; one barrier then separates the staging from the reads, and a
-  // second one the reads from the next round's staging.
-  __shared__ halfx8 kop[kRound][kRetBlocks][kKS][2][32];
+  // two LDS tiles of a chunk's keys (double buffer, see below)
+  __shared__ halfx8 kop[2][kRetBlocks][kKS][2][32];
   __shared__ float nsum[kRows];
 
   // thread t stages float4 column t mod kC4 of rows t / kC4 + (kT / kC4) j
@@ -165,86 +162,90 @@ __global__ __launch_bounds__(64 * kRetWaves) void screen_kernel(const RetrievePa
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
 
-  for (int64_t f0 = 0; f0 < E; f0 += kRound * kFC) {
-    if (f0 > 0) __syncthreads();  // the previous round's tiles have been read
-    // issue every load of the round: keys (prepared entries or fp32 rows),
-    // then the wave's query operands; entries past E or M read as zero
-    halfx8 pk[PREP ? kRound * kPK : 1];
-    float4 kv[PREP ? 1 : kRound * kStage];
+  // Two chunks in flight: chunk c + 1's loads (keys and query operands,
+  // into the other register buffer) are issued before chunk c is staged,
+  // and chunk c + 1 is staged into the other LDS tile, so one barrier per
+  // chunk separates the staging from the reads.
+  struct Chunk {
+    halfx8 pk[PREP ? kPK : 1];
+    float4 kv[PREP ? 1 : kStage];
+    halfx8 aq[kKS];
+  };
+  auto issue = [&](Chunk& ch, int64_t fc) {
+    const int nks = fc < E ? static_cast<int>((E - fc + 15) / 16 < kKS ? (E - fc + 15) / 16 : kKS) : 0;
+    if constexpr (PREP) {
 #pragma unroll
-    for (int c = 0; c < kRound; ++c) {
-      const int64_t fc = f0 + c * kFC;
-      const int nks = fc < E ? static_cast<int>((E - fc + 15) / 16 < kKS ? (E - fc + 15) / 16 : kKS) : 0;
-      if constexpr (PREP) {
+      for (int j = 0; j < kPK; ++j) {
+        const int i = tid + kT * j;
+        const int b = i / (kKS * 64);
+        const int w = i - b * (kKS * 64);
+        const int64_t kb = static_cast<int64_t>(kg) * kRetBlocks + b;
+        if (w < nks * 64 && kb < p.nkb)
+          ch.pk[j] = static_cast<const halfx8*>(p.kop)[(kb * p.nks + fc / 16) * 64 + w];
+        else
+          ch.pk[j] = halfx8{};
+      }
+    } else {
 #pragma unroll
-        for (int j = 0; j < kPK; ++j) {
-          const int i = tid + kT * j;      // entry within the workgroup's chunk
-          const int b = i / (kKS * 64);    // block
-          const int w = i - b * (kKS * 64);
-          const int64_t kb = static_cast<int64_t>(kg) * kRetBlocks + b;
-          if (w < nks * 64 && kb < p.nkb)
-            pk[c * kPK + j] = static_cast<const halfx8*>(p.kop)[(kb * p.nks + fc / 16) * 64 + w];
-          else
-            pk[c * kPK + j] = halfx8{};
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < kStage; ++j) {
-          const int row = srow0 + (kT / kC4) * j;
-          const int64_t e = fc + 4 * c4;
-          const uint32_t off =
-              e < E ? static_cast<uint32_t>((row * E + e) * 4) : kDropOffset;
-          kv[c * kStage + j] =
-              __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
-        }
+      for (int j = 0; j < kStage; ++j) {
+        const int row = srow0 + (kT / kC4) * j;
+        const int64_t e = fc + 4 * c4;
+        const uint32_t off = e < E ? static_cast<uint32_t>((row * E + e) * 4) : kDropOffset;
+        ch.kv[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(kres, off, 0, 0));
       }
     }
-    halfx8 aq[kRound * kKS];
 #pragma unroll
-    for (int i = 0; i < kRound * kKS; ++i) {
-      const int64_t ks = f0 / 16 + i;
-      aq[i] = ks < p.nks ? __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(
-                                                          ores, lane_off,
-                                                          static_cast<uint32_t>(ks) * 1024u, 0))
-                         : halfx8{};
+    for (int i = 0; i < kKS; ++i) {
+      const int64_t ks = fc / 16 + i;
+      ch.aq[i] = ks < p.nks ? __builtin_bit_cast(halfx8, __builtin_amdgcn_raw_buffer_load_b128(
+                                                             ores, lane_off,
+                                                             static_cast<uint32_t>(ks) * 1024u, 0))
+                            : halfx8{};
     }
+  };
+  auto consume = [&](const Chunk& ch, int64_t fc, int slot) {
+    if constexpr (PREP) {
+      halfx8* dst = &kop[slot][0][0][0][0];
 #pragma unroll
-    for (int c = 0; c < kRound; ++c) {
-      if constexpr (PREP) {
-        halfx8* dst = &kop[c][0][0][0][0];
+      for (int j = 0; j < kPK; ++j) dst[tid + kT * j] = ch.pk[j];
+    } else {
 #pragma unroll
-        for (int j = 0; j < kPK; ++j) dst[tid + kT * j] = pk[c * kPK + j];
-      } else {
-#pragma unroll
-        for (int j = 0; j < kStage; ++j) {
-          const int row = srow0 + (kT / kC4) * j;
-          const float4 v = kv[c * kStage + j];
-          n2[j] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2[j]))));
-          const int b = row / kKB;
-          const int r = row % kKB;
-          const int ks = c4 >> 2;
-          const int h = (c4 >> 1) & 1;
-          const int sub = c4 & 1;
-          const int srow = r ^ ((2 * ks + h) & 31);
-          reinterpret_cast<halfx4*>(&kop[c][b][ks][h][srow])[sub] = to_op(v);
-        }
+      for (int j = 0; j < kStage; ++j) {
+        const int row = srow0 + (kT / kC4) * j;
+        const float4 v = ch.kv[j];
+        n2[j] = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, n2[j]))));
+        const int b = row / kKB;
+        const int r = row % kKB;
+        const int ks = c4 >> 2;
+        const int h = (c4 >> 1) & 1;
+        const int sub = c4 & 1;
+        const int srow = r ^ ((2 * ks + h) & 31);
+        reinterpret_cast<halfx4*>(&kop[slot][b][ks][h][srow])[sub] = to_op(v);
       }
     }
     __syncthreads();
     if (active) {
 #pragma unroll
-      for (int c = 0; c < kRound; ++c) {
+      for (int ks = 0; ks < kKS; ++ks) {
+        if (fc + 16 * ks < E) {
+          const int srow = r32 ^ ((2 * ks + half) & 31);
 #pragma unroll
-        for (int ks = 0; ks < kKS; ++ks) {
-          if (f0 + c * kFC + 16 * ks < E) {
-            const int srow = r32 ^ ((2 * ks + half) & 31);
-#pragma unroll
-            for (int b = 0; b < kRetBlocks; ++b)
-              acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kop[c][b][ks][half][srow],
-                                                              aq[c * kKS + ks], acc[b], 0, 0, 0);
-          }
+          for (int b = 0; b < kRetBlocks; ++b)
+            acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kop[slot][b][ks][half][srow], ch.aq[ks],
+                                                            acc[b], 0, 0, 0);
         }
       }
+    }
+  };
+  Chunk ca, cb;
+  issue(ca, 0);
+  for (int64_t f0 = 0; f0 < E; f0 += 2 * kFC) {
+    const bool second = f0 + kFC < E;
+    if (second) issue(cb, f0 + kFC);
+    consume(ca, f0, 0);
+    if (second) {
+      if (f0 + 2 * kFC < E) issue(ca, f0 + 2 * kFC);
+      consume(cb, f0 + kFC, 1);
     }
   }
   if (active) {
