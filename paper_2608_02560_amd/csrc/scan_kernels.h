@@ -438,28 +438,33 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
 #pragma unroll
   for (int n = 0; n < NL; ++n) a2[n] *= -kLog2e;
 
+  // The initial state is read after the first tile's loads are issued: a
+  // row taken from a state store first needs its index, and that round trip
+  // then overlaps the tile's.
   float h[NL];
-  if constexpr (KIND == kSummary) {
-#pragma unroll
-    for (int n = 0; n < NL; ++n) h[n] = 0.f;
-  } else {
-    if (p.nchunks > 1) {
-      load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
-    } else if (p.h0_score != nullptr) {
-      compose_state_wave<NL, TSt>(h, p, b, sofs);
-    } else if (p.flags & kHasH0) {
-      const TSt* src = h0_row<TSt>(p, b);
-      if (src != nullptr) {
-        load_state<NL>(h, src + sofs);
-      } else {
-#pragma unroll
-        for (int n = 0; n < NL; ++n) h[n] = __builtin_nanf("");
-      }
-    } else {
+  auto init_state = [&]() {
+    if constexpr (KIND == kSummary) {
 #pragma unroll
       for (int n = 0; n < NL; ++n) h[n] = 0.f;
+    } else {
+      if (p.nchunks > 1) {
+        load_state<NL>(h, p.carry + (static_cast<int64_t>(b) * p.nchunks + c) * D * N + sofs);
+      } else if (p.h0_score != nullptr) {
+        compose_state_wave<NL, TSt>(h, p, b, sofs);
+      } else if (p.flags & kHasH0) {
+        const TSt* src = h0_row<TSt>(p, b);
+        if (src != nullptr) {
+          load_state<NL>(h, src + sofs);
+        } else {
+#pragma unroll
+          for (int n = 0; n < NL; ++n) h[n] = __builtin_nanf("");
+        }
+      } else {
+#pragma unroll
+        for (int n = 0; n < NL; ++n) h[n] = 0.f;
+      }
     }
-  }
+  };
 
   const float dsk = (kRead && (p.flags & kHasD)) ? p.Dskip[d] : 0.f;
 
@@ -684,8 +689,9 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       if (tile * kPF + k < nsteps) step(tb, k, tile * kPF + k);
   };
 
+  if (nsteps > 0) fetch(t0b, 0);
+  init_state();
   if (nsteps > 0) {
-    fetch(t0b, 0);
     // Tile 0 completes before tile 1 is requested (vmcnt(0); lgkmcnt and
     // expcnt untouched): at launch every wave requests at once, and tile 0
     // then does not queue behind tile 1 (corpus encode 1.2445 -> 1.2297 ms).
