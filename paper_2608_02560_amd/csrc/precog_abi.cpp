@@ -47,7 +47,7 @@ bool valid_n(int64_t n) {
 
 constexpr int64_t kBlock = precog::kScanThreads;  // lanes per scan workgroup (real and complex A)
 constexpr int64_t kTargetWaves = 2048;    // 2 waves per SIMD on 256 CUs
-constexpr int64_t kMinAutoChunk = 64;
+constexpr int64_t kMinAutoChunk = 8;
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
