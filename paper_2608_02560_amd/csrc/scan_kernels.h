@@ -507,10 +507,12 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // and the readout use plain VALU operands instead of DPP broadcasts.  The
   // slice is private to the wave: no barrier.
   // Used where it was measured to pay: with a readout (32 broadcasts per
-  // token replaced), or when a channel spans several lanes (N > 16); a
-  // readout-free N = 16 scan saves only the 16 B broadcasts, less than the
-  // staging costs.
-  constexpr bool kLds = NL == 16 && (kRead || P > 1);
+  // token replaced), when a channel spans several lanes (N > 16), and for
+  // readout-free N = 16 scans over 16-bit inputs in 4-token tiles, whose
+  // staging is one dword per lane (the long-context summary pass: 2.67 ->
+  // 2.64 ms); with per-token staging a readout-free N = 16 scan saves only
+  // the 16 B broadcasts, less than the staging costs.
+  constexpr bool kLds = NL == 16 && (kRead || P > 1 || (sizeof(typename SI::raw) == 2 && kPF == 4));
   // 16-bit coefficients with N = 16 in one lane: a 4-token tile's B (and C)
   // rows are 4 x 16 x 2 bytes = 32 dwords, so lanes 0..31 fetch one dword
   // each (token l / 8, coefficients 2 (l mod 8) and 2 (l mod 8) + 1): one
