@@ -646,7 +646,7 @@ def bench_extensions(args, flush):
         traj = torch.empty((B, L // every, D, N), dtype=torch.float16, device="cuda")
         run = lambda: P.scan_trajectory(desc, inp["x"], inp["dt"], inp["A"], inp["B"], None, None,
                                         None, None, None, None, traj, every)
-        t_ms = time_events(run, 5)
+        t_ms = time_events(run, 5, hold=True)
         nb = scan_bytes(B, L, D, N, readout=False) - B * D * N * 2 + traj.numel() * 2
         traj_res["every_%d" % every] = {"ms": t_ms, "tokens_per_s": B * L / (t_ms * 1e-3),
                                         "states_kept_per_chunk": L // every, **rates(nb, t_ms)}

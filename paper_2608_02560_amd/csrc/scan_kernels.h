@@ -392,7 +392,7 @@ __device__ __forceinline__ float lane_xor(float v, int m) {
 // Every lane of a wave stays active through the time loop (DPP broadcasts
 // read other lanes); lanes past D compute on clamped channels and store
 // nothing.
-template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, bool TRAJ>
+template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, int TRAJ>
 __global__ __launch_bounds__(kSBlock) void scan_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   constexpr int NL = N / P;                // states held by one lane
   constexpr int G = (NL + 15) / 16;        // registers per token for B_t (and C_t)
   constexpr int kChan = kSBlock / P;       // channels per workgroup
-  constexpr int kPF = TRAJ ? kPFWide : kPFPlain;
+  constexpr int kPF = TRAJ != 0 ? kPFWide : kPFPlain;
   constexpr bool kRead = KIND == kReadout;
   const int lb = xcd_remap(blockIdx.x, gridDim.x);
   const int dblk = lb % p.dblocks;
@@ -471,7 +471,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // first captured token at or after t0: the smallest t >= t0 with
   // (t + 1) mod every == 0; slot = its index in the thinned trajectory
   int64_t cd = 0, slot = 0;
-  if constexpr (TRAJ) {
+  if constexpr (TRAJ != 0) {
     const int64_t ev = p.traj_every;
     const int64_t first = (t0 + ev) / ev * ev - 1;
     cd = first - t0;
@@ -631,6 +631,18 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     }
   };
 
+  // fp16 trajectory with 16 states per lane: the wave's 64 state rows
+  // (2 KB, contiguous in traj) go out as two stores that are each contiguous
+  // across the wave, transposed through a wave-private LDS slice: lane l
+  // writes its 32 bytes at 32 l, then reads the 16 bytes at 16 l and at
+  // 1024 + 16 l, which hold half l mod 2 of channels l / 2 and 32 + l / 2
+  // (each store instruction then fills whole lines).  Its own
+  // instantiation (TRAJ == 2), launched where the stores bound the kernel:
+  // every = 1 0.659 -> 0.500 ms, every = 2 0.350 -> 0.308 ms, but every = 4
+  // 0.200 -> 0.249 ms (SMC workload).
+  constexpr bool kTrajT = TRAJ == 2 && P == 1 && NL == 16 && std::is_same<TSt, f16_t>::value;
+  __shared__ __attribute__((aligned(16))) st_half8 traj_lds[kTrajT ? kSBlock / 64 : 1][kTrajT ? 128 : 1];
+  const int nlive = static_cast<int>(D - wave_d0 < 64 ? D - wave_d0 : 64);  // live channels of the wave
   float dtacc = 0.f;
   auto step = [&](const Tile& tb, int k, int st) {
     const float xv = SI::f32(tb.x[k]);
@@ -663,12 +675,22 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       SO::store(ry, dly, static_cast<uint32_t>(st) * out_row, out);
     }
     if constexpr (KIND == kSummary) dtacc += dtv;
-    if constexpr (TRAJ) {
-      if (cd == 0) {
-        if (live)
-          store_state_vec<NL>(static_cast<TSt*>(p.traj) +
-                                  ((static_cast<int64_t>(b) * p.traj_count + slot) * D) * N + sofs,
-                              h);
+    if constexpr (TRAJ != 0) {
+      if (cd == 0) {  // wave-uniform
+        TSt* row = static_cast<TSt*>(p.traj) + (static_cast<int64_t>(b) * p.traj_count + slot) * D * N;
+        if constexpr (kTrajT) {
+          const st_float8 v0 = {h[0], h[1], h[2], h[3], h[4], h[5], h[6], h[7]};
+          const st_float8 v1 = {h[8], h[9], h[10], h[11], h[12], h[13], h[14], h[15]};
+          traj_lds[wave][2 * lane] = __builtin_convertvector(v0, st_half8);
+          traj_lds[wave][2 * lane + 1] = __builtin_convertvector(v1, st_half8);
+          const st_half8 o0 = traj_lds[wave][lane];
+          const st_half8 o1 = traj_lds[wave][64 + lane];
+          TSt* wrow = row + wave_d0 * N;
+          if ((lane >> 1) < nlive) *reinterpret_cast<st_half8*>(wrow + 8 * lane) = o0;
+          if (32 + (lane >> 1) < nlive) *reinterpret_cast<st_half8*>(wrow + 512 + 8 * lane) = o1;
+        } else if (live) {
+          store_state_vec<NL>(row + sofs, h);
+        }
         ++slot;
         cd = p.traj_every - 1;
       } else {
@@ -767,23 +789,16 @@ __global__ __launch_bounds__(256) void carry_kernel(const ScanParams p, int N) {
   }
 }
 
-template <int N, typename TIn, typename TOut, typename TSt, bool TRAJ>
-hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
-  const int64_t rows_blocks = static_cast<int64_t>(p.dblocks) * p.B;
+// The final pass: readout (with or without gate) or state-only, with the
+// trajectory mode TRAJ (0 none, 1 direct stores, 2 stores transposed
+// through LDS).
+template <int N, typename TIn, typename TOut, typename TSt, int TRAJ>
+hipError_t launch_final(const ScanParams& p, int64_t g3, hipStream_t s) {
   const TIn* X = static_cast<const TIn*>(p.x);
   const TIn* DT = static_cast<const TIn*>(p.dt);
   const TIn* Z = static_cast<const TIn*>(p.z);
   const TIn* BB = static_cast<const TIn*>(p.Bm);
   const TIn* CC = static_cast<const TIn*>(p.Cm);
-  if (p.nchunks > 1) {
-    const int64_t g1 = rows_blocks * (p.nchunks - 1);
-    hipLaunchKernelGGL((scan_kernel<N, TIn, float, float, kSummary, false, false>), dim3(static_cast<unsigned>(g1)),
-                       dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
-    const int64_t lanes = p.B * p.D * N;
-    hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
-                       0, s, p, N);
-  }
-  const int64_t g3 = rows_blocks * p.nchunks;
   if (p.y != nullptr && (p.flags & kHasZ))
     hipLaunchKernelGGL((scan_kernel<N, TIn, TOut, TSt, kReadout, true, TRAJ>), dim3(static_cast<unsigned>(g3)),
                        dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<TOut*>(p.y), p);
@@ -794,6 +809,32 @@ hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
     hipLaunchKernelGGL((scan_kernel<N, TIn, float, TSt, kStateOnly, false, TRAJ>), dim3(static_cast<unsigned>(g3)),
                        dim3(kSBlock), 0, s, X, DT, Z, BB, CC, static_cast<float*>(nullptr), p);
   return hipGetLastError();
+}
+
+template <int N, typename TIn, typename TOut, typename TSt, bool TRAJ>
+hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
+  const int64_t rows_blocks = static_cast<int64_t>(p.dblocks) * p.B;
+  if (p.nchunks > 1) {
+    const int64_t g1 = rows_blocks * (p.nchunks - 1);
+    hipLaunchKernelGGL((scan_kernel<N, TIn, float, float, kSummary, false, 0>), dim3(static_cast<unsigned>(g1)),
+                       dim3(kSBlock), 0, s, static_cast<const TIn*>(p.x), static_cast<const TIn*>(p.dt),
+                       static_cast<const TIn*>(p.z), static_cast<const TIn*>(p.Bm),
+                       static_cast<const TIn*>(p.Cm), static_cast<float*>(nullptr), p);
+    const int64_t lanes = p.B * p.D * N;
+    hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
+                       0, s, p, N);
+  }
+  const int64_t g3 = rows_blocks * p.nchunks;
+  if constexpr (!TRAJ) {
+    return launch_final<N, TIn, TOut, TSt, 0>(p, g3, s);
+  } else {
+    // fp16 trajectories of 16 states per lane captured every token or every
+    // other token: the store-bound case, transposed stores
+    if constexpr (N == 16 && std::is_same<TSt, f16_t>::value) {
+      if (p.traj_every <= 2) return launch_final<N, TIn, TOut, TSt, 2>(p, g3, s);
+    }
+    return launch_final<N, TIn, TOut, TSt, 1>(p, g3, s);
+  }
 }
 
 template <int N, typename TIn, typename TOut, bool TRAJ>
