@@ -75,6 +75,38 @@ def test_trajectory_bf16_fp16_state_only():
         assert err_rms(traj.double().cpu().numpy(), ref) <= TOL_BF16
 
 
+@pytest.mark.parametrize("every,readout", [(1, False), (2, False), (1, True), (2, True)])
+def test_trajectory_fp16_partial_wave(every, readout):
+    """fp16 trajectories captured every token or every other token (stores
+    transposed through LDS) with D = 200 = 3 x 64 + 8: the last wave of each
+    row has 8 live channels.  Every captured state matches the oracle, the
+    last one equals hT bit for bit, and a NaN guard past the end of the
+    trajectory buffer is untouched."""
+    Bt, L, D, N = 3, 40, 200, 16
+    inp = synth.scan_inputs_host(Bt, L, D, N, seed=90 + every, in_dtype=torch.bfloat16)
+    d = _dev(inp)
+    slots = L // every
+    n = Bt * slots * D * N
+    guard = 4096
+    buf = torch.full((n + guard,), float("nan"), dtype=torch.float16, device=DEV)
+    traj = buf[:n].view(Bt, slots, D, N)
+    hT = torch.empty((Bt, D, N), dtype=torch.float16, device=DEV)
+    y = torch.empty((Bt, L, D), dtype=torch.float32, device=DEV) if readout else None
+    # few channels: the automatic chunking cuts time (the capture runs in
+    # the replay pass)
+    desc = P.scan_desc(Bt, L, D, N, P.BF16, P.F32, P.F16)
+    nws = P.scan_workspace_bytes(desc)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=DEV)
+    P.scan_trajectory(desc, d["x"], d["dt"], d["A"], d["B"], d["C"] if readout else None,
+                      d["z"] if readout else None, d["Dskip"] if readout else None, None, y, hT,
+                      traj, every, ws, nws)
+    torch.cuda.synchronize()
+    assert torch.isnan(buf[n:]).all()
+    ref = _ref_traj(inp, every)
+    assert err_rms(traj.double().cpu().numpy(), ref) <= TOL_BF16
+    assert torch.equal(traj[:, -1], hT)
+
+
 def test_trajectory_empty_and_validation():
     inp = synth.scan_inputs_host(1, 5, 64, 16, seed=83, in_dtype=torch.float32)
     d = _dev(inp)
