@@ -407,12 +407,22 @@ def bench_query_path(args, flush):
         P.scan_encode(desc, inp["x"], inp["dt"], inp["A"], inp["B"], inp["C"], inp["z"],
                       inp["Dskip"], h0, y, hT)
 
+    nq = P.query_workspace_bytes(desc, M, E)
+    wq = torch.empty(max(nq, 16), dtype=torch.uint8, device="cuda")
+
+    def one_call(prep=None):
+        P.query_top1_prefill(desc, q, K, store3, idx, inp["x"], inp["dt"], inp["A"], inp["B"],
+                             inp["C"], inp["z"], inp["Dskip"], y, hT, wq, nq, prepared=prep)
+
     r_ms = time_events(retrieve, 20, flush, hold=True)
     p_ms = time_events(prefill, 20, flush, hold=True)
     f_ms = time_events(fused, 20, flush, hold=True)
     fw_ms = time_events(fused, 20, None, hold=True)
     fp_ms = time_events(fused_prepared, 20, flush, hold=True)
     s_ms = time_events(separate, 20, flush, hold=True)
+    o_ms = time_events(one_call, 20, flush, hold=True)
+    ow_ms = time_events(one_call, 20, None, hold=True)
+    op_ms = time_events(lambda: one_call(prepared), 20, flush, hold=True)
     flops = 2.0 * Q * M * E
     rbytes = (Q + M) * E * 4 + Q * 4
     pbytes = scan_bytes(Q, Lq, D, N, h0_bytes=2)  # the injected rows are read once
@@ -424,12 +434,17 @@ def bench_query_path(args, flush):
            "end_to_end_fused_top1_warm_us": fw_ms * 1e3,
            "end_to_end_fused_top1_prepared_index_us": fp_ms * 1e3,
            "end_to_end_separate_gather_us": s_ms * 1e3,
+           "one_call_top1_us": o_ms * 1e3,
+           "one_call_top1_warm_us": ow_ms * 1e3,
+           "one_call_top1_prepared_index_us": op_ms * 1e3,
+           "one_call": "precog_query_top1_prefill: retrieval, then the decision and the "
+                       "prefill from the decided row in one launch",
            "retrieve_top1_us": r_ms * 1e3,
            "retrieve_bytes": rbytes, "retrieve_gbps": rbytes / (r_ms * 1e-3) / 1e9,
            "retrieve_mfma_frac": flops / (r_ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS,
            "prefill_indexed_us": p_ms * 1e3,
-           "queries_per_s": Q / (f_ms * 1e-3)}
-    res.update(rates(rbytes + pbytes, f_ms))
+           "queries_per_s": Q / (o_ms * 1e-3)}
+    res.update(rates(rbytes + pbytes, o_ms))
     res["prefill_gbps"] = pbytes / (p_ms * 1e-3) / 1e9
     res["prefill_hbm_frac"] = res["prefill_gbps"] / HBM_PEAK_GBPS
     if not args.no_cpu:
@@ -454,7 +469,7 @@ def bench_query_path(args, flush):
             out["prefill_ms_" + name] = (t3 - t2) * 1e3
         res["oracle"] = out
         del store_h, a
-    del inp, y, hT, h0, store, ws, q, K, prepared
+    del inp, y, hT, h0, store, ws, wq, q, K, prepared
     torch.cuda.empty_cache()
     return res
 

@@ -343,6 +343,48 @@ precog_status precog_retrieve_topk_prepared(const float *query_emb,
                                             size_t workspace_bytes,
                                             void *stream);
 
+/* The whole query-time path of Sec. 4.2 in one call: the exact top-1
+ * retrieval, the injection of the retrieved state and the query prefill
+ * from it (Eq. 1; Theorem 1 of Sec. 4.3 is why the prefill from the stored
+ * state equals processing chunk and query together):
+ *   idx[b] = the top-1 of precog_retrieve_top1 (or, with `prepared`, of
+ *            precog_retrieve_topk_prepared with k = 1) for query_emb row b,
+ *   then exactly precog_scan_encode_indexed(desc, x, dt, A, B, C, z, Dskip,
+ *            state_store, M, idx, NULL, 1, 1.0, y, hT, ...).
+ * idx, y and hT are bitwise those of the two calls.  Batch row b of the scan
+ * is query b (desc->batch = Q); the store has one state row per key of the
+ * index (M rows of [D, N] at stride desc->h0_batch_stride, 0 = D*N, in
+ * desc->state_dtype).  With N = 16, bf16 inputs, one pass over time (the
+ * automatic chunking picks one when batch x channels fill the GPU, or
+ * desc->chunk >= L) and y with a gate (or y NULL), each prefill workgroup
+ * decides its own query in one wave while the other waves fetch their first
+ * tokens, then starts from the decided row (one launch for the decision,
+ * injection and prefill); otherwise the retrieval's decision and the
+ * prefill run as two launches.
+ *   query_emb  [Q, E] fp32    index_emb [M, E] fp32 (as precog_retrieve_top1)
+ *   prepared   NULL, or the prepared index of index_emb (precog_retrieve_prepare)
+ *              with prepared_bytes >= precog_retrieve_index_bytes(M, E)
+ *              (else PRECOG_ERR_WORKSPACE)
+ *   state_store  [M, D, N] rows as above; NULL only when M == 0
+ *   idx        [Q] int32 output (M == 0 gives -1 and NaN start states)
+ *   x ... hT   as precog_scan_encode
+ *   workspace  precog_query_workspace_bytes(desc, M, E) bytes, 16-byte aligned.
+ * Every argument of both halves is validated before anything is launched;
+ * the status codes are those of the two calls. */
+size_t precog_query_workspace_bytes(const precog_scan_desc *desc, int64_t M, int64_t E);
+precog_status precog_query_top1_prefill(const precog_scan_desc *desc,
+                                        const float *query_emb,
+                                        const float *index_emb,
+                                        const void *prepared,
+                                        size_t prepared_bytes, int64_t M,
+                                        int64_t E, const void *state_store,
+                                        int32_t *idx, const void *x,
+                                        const void *dt, const float *A,
+                                        const void *B, const void *C,
+                                        const void *z, const float *Dskip,
+                                        void *y, void *hT, void *workspace,
+                                        size_t workspace_bytes, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* State injection                                                          */
 /* ------------------------------------------------------------------------ */

@@ -168,10 +168,16 @@ struct StoreStart {
   double tau;
 };
 
-precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, const float* A,
-                   const void* B, const void* C, const void* z, const float* Dskip,
-                   const void* h0, const StoreStart& from, void* y, void* hT, void* traj,
-                   int64_t every, void* workspace, size_t workspace_bytes, void* stream) {
+// Validates a scan call and fills `p` for its launch; `launch` is false when
+// there is nothing to compute (the call returns PRECOG_OK without launching).
+// Nothing is launched here.
+precog_status scan_prepare(const precog_scan_desc* desc, const void* x, const void* dt,
+                           const float* A, const void* B, const void* C, const void* z,
+                           const float* Dskip, const void* h0, const StoreStart& from, void* y,
+                           void* hT, void* traj, int64_t every, void* workspace,
+                           size_t workspace_bytes, precog::ScanParams& p, bool& launch,
+                           bool dev_check = true) {
+  launch = false;
   const int32_t* h0_idx = from.idx;
   const int64_t h0_rows = from.rows;
   precog_status st = validate_desc(desc);
@@ -205,10 +211,11 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   if (Bt * D * N / 256 + 1 > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
 
   int cus = 1;
+  if (!dev_check) return PRECOG_OK;  // arguments checked, nothing prepared
   st = check_device(&cus);
   if (st != PRECOG_OK) return st;
 
-  precog::ScanParams p{};
+  p = precog::ScanParams{};
   p.x = x;
   p.dt = dt;
   p.z = y ? z : nullptr;
@@ -246,15 +253,30 @@ precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, 
   p.traj_every = traj ? every : 1;
   p.traj_count = traj_count;
   if (!p.y && !p.hT && traj_count == 0) return PRECOG_OK;  // L == 0 and no state requested
+  launch = true;
+  return PRECOG_OK;
+}
 
+hipError_t scan_launch(const precog_scan_desc* desc, const precog::ScanParams& p, void* stream) {
+  const int N = static_cast<int>(desc->dstate);
+  return p.traj_count > 0
+             ? precog::launch_scan_traj(p, N, desc->in_dtype, desc->out_dtype, desc->state_dtype,
+                                        static_cast<hipStream_t>(stream))
+             : precog::launch_scan(p, N, desc->in_dtype, desc->out_dtype, desc->state_dtype,
+                                   static_cast<hipStream_t>(stream));
+}
+
+precog_status scan(const precog_scan_desc* desc, const void* x, const void* dt, const float* A,
+                   const void* B, const void* C, const void* z, const float* Dskip,
+                   const void* h0, const StoreStart& from, void* y, void* hT, void* traj,
+                   int64_t every, void* workspace, size_t workspace_bytes, void* stream) {
+  precog::ScanParams p;
+  bool launch = false;
+  const precog_status st = scan_prepare(desc, x, dt, A, B, C, z, Dskip, h0, from, y, hT, traj,
+                                        every, workspace, workspace_bytes, p, launch);
+  if (st != PRECOG_OK || !launch) return st;
   (void)hipGetLastError();
-  const hipError_t e =
-      traj_count > 0
-          ? precog::launch_scan_traj(p, static_cast<int>(N), desc->in_dtype, desc->out_dtype,
-                                     desc->state_dtype, static_cast<hipStream_t>(stream))
-          : precog::launch_scan(p, static_cast<int>(N), desc->in_dtype, desc->out_dtype,
-                                desc->state_dtype, static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
+  return scan_launch(desc, p, stream) == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 }  // namespace
 
@@ -378,16 +400,17 @@ precog_status precog_retrieve_prepare(const float* index_emb, int64_t M, int64_t
 }  // extern "C"
 
 namespace precog {
-precog_status retrieve_entry(const float* query_emb, const float* index_emb, const void* prepared,
+precog_status retrieve_setup(const float* query_emb, const float* index_emb, const void* prepared,
                              int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
                              double* score, void* workspace, size_t workspace_bytes,
-                             void* stream) {
+                             RetrieveParams& p, bool dev_check) {
   if (Q < 0 || M < 0 || E < 4 || E > 4096) return PRECOG_ERR_SHAPE;
   if (E % 4 != 0) return PRECOG_ERR_ALIGN;
   if (Q > 0x7fffffffLL || M > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
   // screen workgroups (at most one per 32 keys and 128 queries) and the
   // workspace sizes must stay within their integer types
   if (ceil_div(M, 32) * ceil_div(Q, 128) > 0x7fffffffLL) return PRECOG_ERR_SHAPE;
+  p = RetrieveParams{};
   if (Q == 0) return PRECOG_OK;
   if (!query_emb || !idx) return PRECOG_ERR_NULL;
   if (M > 0 && !index_emb) return PRECOG_ERR_NULL;
@@ -396,10 +419,10 @@ precog_status retrieve_entry(const float* query_emb, const float* index_emb, con
     if (p && !aligned16(p)) return PRECOG_ERR_ALIGN;
   const size_t need = precog_retrieve_workspace_bytes(Q, M, E);
   if (M > 0 && (!workspace || workspace_bytes < need)) return PRECOG_ERR_WORKSPACE;
+  if (!dev_check) return PRECOG_OK;  // arguments checked, nothing prepared
   const precog_status st = check_device();
   if (st != PRECOG_OK) return st;
 
-  precog::RetrieveParams p{};
   const RetrieveWs w = retrieve_ws(Q, M, E);
   char* ws = static_cast<char*>(workspace);
   p.q = query_emb;
@@ -435,6 +458,17 @@ precog_status retrieve_entry(const float* query_emb, const float* index_emb, con
                            precog::kRetWaves);
   p.nks = static_cast<int>((E + 15) / 16);
   p.k = static_cast<int>(k);
+  return PRECOG_OK;
+}
+
+precog_status retrieve_entry(const float* query_emb, const float* index_emb, const void* prepared,
+                             int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
+                             double* score, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  RetrieveParams p;
+  const precog_status st = retrieve_setup(query_emb, index_emb, prepared, Q, M, E, k, idx, score,
+                                          workspace, workspace_bytes, p, true);
+  if (st != PRECOG_OK || Q == 0) return st;
   (void)hipGetLastError();
   const hipError_t e = precog::launch_retrieve(p, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
@@ -468,6 +502,60 @@ precog_status precog_retrieve_topk_prepared(const float* query_emb, const float*
   if (prepared_bytes < precog_retrieve_index_bytes(M, E)) return PRECOG_ERR_WORKSPACE;
   return precog::retrieve_entry(query_emb, index_emb, prepared, Q, M, E, k, idx, score, workspace,
                   workspace_bytes, stream);
+}
+
+size_t precog_query_workspace_bytes(const precog_scan_desc* desc, int64_t M, int64_t E) {
+  if (validate_desc(desc) != PRECOG_OK) return 0;
+  const size_t r = precog_retrieve_workspace_bytes(desc->batch, M, E);
+  if (r == 0) return 0;
+  return align_up(r) + precog_scan_workspace_bytes(desc);
+}
+
+// Retrieval workspace first, then the scan's (time chunks only), 256-byte
+// aligned.
+precog_status precog_query_top1_prefill(const precog_scan_desc* desc, const float* query_emb,
+                                        const float* index_emb, const void* prepared,
+                                        size_t prepared_bytes, int64_t M, int64_t E,
+                                        const void* state_store, int32_t* idx, const void* x,
+                                        const void* dt, const float* A, const void* B,
+                                        const void* C, const void* z, const float* Dskip,
+                                        void* y, void* hT, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  precog_status st = validate_desc(desc);
+  if (st != PRECOG_OK) return st;
+  const int64_t Q = desc->batch;
+  if (prepared && prepared_bytes < precog_retrieve_index_bytes(M, E)) return PRECOG_ERR_WORKSPACE;
+  const size_t rbytes = precog_retrieve_workspace_bytes(Q, M, E);
+  const size_t roff = align_up(rbytes);
+  void* sws = workspace && workspace_bytes > roff ? static_cast<char*>(workspace) + roff : nullptr;
+  const size_t sbytes = workspace_bytes > roff ? workspace_bytes - roff : 0;
+  const StoreStart from{idx, M, nullptr, 1, 1.0};
+  precog::RetrieveParams rp;
+  precog::ScanParams p;
+  bool launch = false;
+  // every argument of both halves first, then the device
+  for (const bool dev : {false, true}) {
+    st = precog::retrieve_setup(query_emb, index_emb, prepared, Q, M, E, 1, idx, nullptr,
+                                workspace, workspace_bytes, rp, dev);
+    if (st != PRECOG_OK || Q == 0) return st;
+    st = scan_prepare(desc, x, dt, A, B, C, z, Dskip, state_store, from, y, hT, nullptr, 1, sws,
+                      sbytes, p, launch, dev);
+    if (st != PRECOG_OK) return st;
+  }
+  (void)hipGetLastError();
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = precog::launch_retrieve_screen(rp, s);
+  if (e == hipSuccess) {
+    const bool fused = launch && desc->dstate == 16 && desc->in_dtype == PRECOG_BF16 &&
+                       p.nchunks == 1 && (p.y == nullptr || (p.flags & precog::kHasZ));
+    if (fused) {
+      e = precog::launch_query_scan(p, rp, desc->out_dtype, desc->state_dtype, s);
+    } else {
+      e = precog::launch_retrieve_decide(rp, s);
+      if (e == hipSuccess && launch) e = scan_launch(desc, p, stream);
+    }
+  }
+  return e == hipSuccess ? PRECOG_OK : PRECOG_ERR_HIP;
 }
 
 precog_status precog_inject_gather(const void* state_store, precog_dtype store_dtype, int64_t M,

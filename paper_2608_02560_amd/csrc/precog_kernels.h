@@ -94,8 +94,25 @@ constexpr int kRetWaves = 8;
 constexpr int kRetBlocks = 2;
 constexpr int kMaxTopK = 64;
 hipError_t launch_retrieve(const RetrieveParams& p, hipStream_t s);
+// The two halves of launch_retrieve: query operands and screen (also sets
+// p's error-bound constants), then the decision.
+hipError_t launch_retrieve_screen(RetrieveParams& p, hipStream_t s);
+hipError_t launch_retrieve_decide(const RetrieveParams& p, hipStream_t s);
+// The query-time prefill that decides its own query's top-1 (batch row b =
+// query b of `rp`, whose screen has run) and starts from that store row:
+// N = 16, bf16 inputs, one pass, readout with gate or state only.  Returns
+// hipErrorInvalidValue for any other configuration, without launching.
+hipError_t launch_query_scan(const ScanParams& p, const RetrieveParams& rp, int out_dtype,
+                             int state_dtype, hipStream_t s);
 // Body of the retrieval entry points (precog_abi.cpp): validates the
 // arguments, lays out `workspace` and launches; `prepared` may be null.
+// Validation and parameters of a retrieval call (nothing launched); with
+// Q == 0 it returns PRECOG_OK and p is not used.  Without dev_check it stops
+// after the argument checks (no device query, p not filled).
+precog_status retrieve_setup(const float* query_emb, const float* index_emb, const void* prepared,
+                             int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
+                             double* score, void* workspace, size_t workspace_bytes,
+                             RetrieveParams& p, bool dev_check);
 precog_status retrieve_entry(const float* query_emb, const float* index_emb, const void* prepared,
                              int64_t Q, int64_t M, int64_t E, int64_t k, int32_t* idx,
                              double* score, void* workspace, size_t workspace_bytes,

@@ -40,6 +40,7 @@
 #include <utility>
 
 #include "compose.h"
+#include "decide.h"
 #include "precog_kernels.h"
 
 namespace precog {
@@ -166,6 +167,12 @@ __device__ __forceinline__ const TSt* h0_row(const ScanParams& p, int64_t b) {
     row = p.h0_idx[b];
     if (row < 0 || row >= p.h0_rows) return nullptr;
   }
+  return static_cast<const TSt*>(p.h0) + row * p.h0_stride;
+}
+// The same for a store row already known to the workgroup.
+template <typename TSt>
+__device__ __forceinline__ const TSt* store_row(const ScanParams& p, int64_t row) {
+  if (row < 0 || row >= p.h0_rows) return nullptr;
   return static_cast<const TSt*>(p.h0) + row * p.h0_stride;
 }
 
@@ -392,11 +399,17 @@ __device__ __forceinline__ float lane_xor(float v, int m) {
 // Every lane of a wave stays active through the time loop (DPP broadcasts
 // read other lanes); lanes past D compute on clamped channels and store
 // nothing.
-template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, int TRAJ>
-__global__ __launch_bounds__(kSBlock) void scan_kernel(
+// DEC (the query-time prefill, one pass, a store row per batch row): batch
+// row b is query b of the retrieval `rp`; wave 0 of the workgroup first
+// decides the query's exact top-1 (decide_query, which also writes it to
+// rp.idx), and the workgroup starts from that store row: one launch instead
+// of the decide and the prefill.  The results are those of the two
+// launches, bit for bit.
+template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, int TRAJ, bool DEC>
+__device__ __forceinline__ void scan_body(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
-    const ScanParams p) {
+    const ScanParams& p, const RetrieveParams* rp) {
   // P lanes share a channel when N > 16, one 16-state group each; group g
   // occupies DPP rows with (row mod P) == g, so every lane of a row needs the
   // same coefficients B_t[16 g + m] / C_t[16 g + m] from its row's lane m.
@@ -422,7 +435,10 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   const bool fair = balance_enabled(p);
   __shared__ int progress[kSWaves];
   if (fair) balance_init(progress, wave);  // uniform over the workgroup
-  if (wave_d0 >= D) return;  // whole wave past the last channel
+  // whole wave past the last channel (DEC: wave 0 never is; the others
+  // leave before the decision's barrier, which then waits for the waves
+  // still running)
+  if (wave_d0 >= D) return;
   const int64_t dtrue = wave_d0 + (lane & 15) + 16 * (lane / (16 * P));
   const bool live = dtrue < D;
   const int64_t d = live ? dtrue : D - 1;
@@ -442,6 +458,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
   // row taken from a state store first needs its index, and that round trip
   // then overlaps the tile's.
   float h[NL];
+  int64_t row_known = 0;  // DEC: the decided store row
   auto init_state = [&]() {
     if constexpr (KIND == kSummary) {
 #pragma unroll
@@ -452,7 +469,7 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       } else if (p.h0_score != nullptr) {
         compose_state_wave<NL, TSt>(h, p, b, sofs);
       } else if (p.flags & kHasH0) {
-        const TSt* src = h0_row<TSt>(p, b);
+        const TSt* src = DEC ? store_row<TSt>(p, row_known) : h0_row<TSt>(p, b);
         if (src != nullptr) {
           load_state<NL>(h, src + sofs);
         } else {
@@ -713,8 +730,26 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
       if (tile * kPF + k < nsteps) step(tb, k, tile * kPF + k);
   };
 
-  if (nsteps > 0) fetch(t0b, 0);
-  init_state();
+  if constexpr (DEC) {
+    // Wave 0 decides while the others wait; then every wave requests its
+    // first tile and its start state.  (Requesting the other waves' first
+    // tiles, and speculatively the store row of the key with the largest
+    // screen score, during the decision was measured to gain nothing: those
+    // loads slowed the decision's own round trips as much as they saved.)
+    __shared__ DecideShared dsh;
+    __shared__ int32_t dec_row;
+    if (wave == 0) {
+      const int32_t r = decide_query(*rp, b, dsh);
+      if (lane == 0) dec_row = r;
+    }
+    __syncthreads();
+    row_known = dec_row;
+    if (nsteps > 0) fetch(t0b, 0);
+    init_state();
+  } else {
+    if (nsteps > 0) fetch(t0b, 0);
+    init_state();
+  }
   if (nsteps > 0) {
     // Tile 0 completes before tile 1 is requested (vmcnt(0); lgkmcnt and
     // expcnt untouched): at launch every wave requests at once, and tile 0
@@ -743,6 +778,25 @@ __global__ __launch_bounds__(kSBlock) void scan_kernel(
     if ((p.flags & kHasHT) && c == p.nchunks - 1)
       store_state<NL>(static_cast<TSt*>(p.hT) + b * p.hT_stride + sofs, h);
   }
+}
+
+template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, int TRAJ>
+__global__ __launch_bounds__(kSBlock) void scan_kernel(
+    const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
+    const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
+    const ScanParams p) {
+  scan_body<N, TIn, TOut, TSt, KIND, HASZ, TRAJ, false>(xg, dtg, zg, Bg, Cg, yg, p, nullptr);
+}
+
+// The query-time prefill with its decision (DEC above).  At most 128 VGPRs
+// (four waves per SIMD, as the plain prefill), so that a 4096-wave prefill
+// still runs in one round; the decision's registers fit in that budget.
+template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ>
+__global__ __launch_bounds__(kSBlock) __attribute__((amdgpu_waves_per_eu(4))) void query_scan_kernel(
+    const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
+    const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
+    const ScanParams p, const RetrieveParams rp) {
+  scan_body<N, TIn, TOut, TSt, KIND, HASZ, 0, true>(xg, dtg, zg, Bg, Cg, yg, p, &rp);
 }
 
 // Pass 2: per (b, d, n) lane, fold the chunk summaries in time order.

@@ -30,7 +30,8 @@ EXPORTS = ("precog_scan_workspace_bytes", "precog_scan_encode", "precog_scan_enc
            "precog_retrieve_workspace_bytes", "precog_retrieve_top1",
            "precog_retrieve_top1_noalloc",
            "precog_retrieve_topk", "precog_retrieve_index_bytes", "precog_retrieve_prepare",
-           "precog_retrieve_topk_prepared", "precog_inject_gather", "precog_inject_compose",
+           "precog_retrieve_topk_prepared", "precog_query_workspace_bytes",
+           "precog_query_top1_prefill", "precog_inject_gather", "precog_inject_compose",
            "precog_inject_fuse",
            "precog_smc_route", "precog_smc_consolidate", "precog_status_string")
 
@@ -92,6 +93,11 @@ def lib():
         L.precog_retrieve_topk_prepared.argtypes = [vp, vp, vp, sz, i64, i64, i64, i64, vp, vp, vp,
                                                     sz, vp]
         L.precog_retrieve_topk_prepared.restype = ctypes.c_int
+        L.precog_query_workspace_bytes.argtypes = [ctypes.POINTER(ScanDesc), i64, i64]
+        L.precog_query_workspace_bytes.restype = sz
+        L.precog_query_top1_prefill.argtypes = [ctypes.POINTER(ScanDesc), vp, vp, vp, sz, i64, i64,
+                                                vp, vp] + [vp] * 9 + [vp, sz, vp]
+        L.precog_query_top1_prefill.restype = ctypes.c_int
         L.precog_inject_gather.argtypes = [vp, ctypes.c_int, i64, i64, vp, i64, vp,
                                            ctypes.c_int, vp]
         L.precog_inject_gather.restype = ctypes.c_int
@@ -258,6 +264,27 @@ def retrieve_topk_prepared(query, index, prepared, k, idx, score, workspace, wor
     _check("precog_retrieve_topk_prepared", st)
 
 
+def query_workspace_bytes(desc: ScanDesc, M, E) -> int:
+    return int(lib().precog_query_workspace_bytes(ctypes.byref(desc), int(M), int(E)))
+
+
+def query_top1_prefill(desc: ScanDesc, query, index, store, idx, x, dt, A, B, C=None, z=None,
+                       Dskip=None, y=None, hT=None, workspace=None, workspace_bytes=None,
+                       prepared=None, stream=None):
+    """precog_query_top1_prefill: exact top-1 of each query, then the prefill
+    of batch row b from store row idx[b] (one call)."""
+    M, E = index.shape
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    pbytes = prepared.numel() * prepared.element_size() if prepared is not None else 0
+    st = lib().precog_query_top1_prefill(ctypes.byref(desc), _ptr(query), _ptr(index),
+                                         _ptr(prepared), int(pbytes), int(M), int(E), _ptr(store),
+                                         _ptr(idx), _ptr(x), _ptr(dt), _ptr(A), _ptr(B), _ptr(C),
+                                         _ptr(z), _ptr(Dskip), _ptr(y), _ptr(hT), _ptr(workspace),
+                                         int(workspace_bytes), _stream(stream))
+    _check("precog_query_top1_prefill", st)
+
+
 def inject_compose(store, idx, score, tau, h0, stream=None):
     M = store.shape[0]
     S = store[0].numel() if M > 0 else h0[0].numel()
@@ -351,6 +378,26 @@ def scan_from_store(x, dt, A, B, store, idx, C=None, z=None, Dskip=None, *, scor
     scan_encode_indexed(desc, x, dt, A, B, C, z, Dskip, store, store.shape[0], idx, y, hT, ws,
                         nbytes, stream, h0_score=score, k=k, tau=tau)
     return y, hT
+
+
+def query_prefill(query, index, store, x, dt, A, B, C=None, z=None, Dskip=None, *,
+                  prepared=None, out_dtype=torch.float32, want_y=True, want_hT=True, chunk=0,
+                  stream=None):
+    """The query-time path in one call: idx = exact top-1 of each query row
+    over index, then the scan of batch row b from store[idx[b]] (store
+    [M, D, N] in the state dtype); returns (idx, y, hT)."""
+    Bt, L, D = x.shape
+    N = A.shape[1]
+    M, E = index.shape
+    desc = scan_desc(Bt, L, D, N, _DT[x.dtype], _DT[out_dtype], _DT[store.dtype], 0, 0, chunk)
+    idx = torch.empty(Bt, dtype=torch.int32, device=x.device)
+    y = torch.empty((Bt, L, D), dtype=out_dtype, device=x.device) if want_y else None
+    hT = torch.empty((Bt, D, N), dtype=store.dtype, device=x.device) if want_hT else None
+    nbytes = query_workspace_bytes(desc, M, E)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=x.device)
+    query_top1_prefill(desc, query, index, store, idx, x, dt, A, B, C, z, Dskip, y, hT, ws, nbytes,
+                       prepared, stream)
+    return idx, y, hT
 
 
 def trajectory(x, dt, A, B, every, C=None, z=None, Dskip=None, h0=None, *,

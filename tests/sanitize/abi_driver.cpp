@@ -154,6 +154,30 @@ int main() {
   EXPECT(precog_retrieve_topk_prepared(FF, FF, nullptr, nb, 4, 10, 16, 3, static_cast<int32_t*>(F),
                                        static_cast<double*>(F), F, rws, nullptr),
          PRECOG_ERR_NULL);
+  // the query-time path in one call: both halves' arguments are checked
+  {
+    const precog_scan_desc qd = desc(4, 16, 64, 16);
+    const size_t qws = precog_query_workspace_bytes(&qd, 10, 16);
+    if (qws < rws) ++failures;
+    EXPECT(precog_query_top1_prefill(&qd, FF, FF, nullptr, 0, 10, 16, F, static_cast<int32_t*>(F),
+                                     F, F, FF, F, F, F, FF, F, F, F, qws - 1, nullptr),
+           PRECOG_ERR_WORKSPACE);
+    EXPECT(precog_query_top1_prefill(&qd, FF, FF, nullptr, 0, 10, 16, nullptr,
+                                     static_cast<int32_t*>(F), F, F, FF, F, F, F, FF, F, F, F, qws,
+                                     nullptr),
+           PRECOG_ERR_NULL);
+    EXPECT(precog_query_top1_prefill(&qd, FF, FF, F, nb - 1, 10, 16, F, static_cast<int32_t*>(F),
+                                     F, F, FF, F, F, F, FF, F, F, F, qws, nullptr),
+           PRECOG_ERR_WORKSPACE);
+    EXPECT(precog_query_top1_prefill(&qd, FF, FF, nullptr, 0, big, 16, F, static_cast<int32_t*>(F),
+                                     F, F, FF, F, F, F, FF, F, F, F, qws, nullptr),
+           PRECOG_ERR_SHAPE);
+    const precog_scan_desc q0 = desc(0, 16, 64, 16);
+    EXPECT(precog_query_top1_prefill(&q0, nullptr, nullptr, nullptr, 0, 10, 16, nullptr, nullptr,
+                                     nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                     nullptr, nullptr, nullptr, 0, nullptr),
+           PRECOG_OK);
+  }
   // injection
   EXPECT(precog_inject_gather(F, PRECOG_BF16, 10, 64, FI, 3, F, PRECOG_F32, nullptr),
          PRECOG_ERR_DTYPE);

@@ -24,6 +24,13 @@ hipError_t launch_scan_complex(const ScanParams&, int, int, int, int, hipStream_
   return reached("scan_complex");
 }
 hipError_t launch_retrieve(const RetrieveParams&, hipStream_t) { return reached("retrieve"); }
+hipError_t launch_retrieve_screen(RetrieveParams&, hipStream_t) { return reached("retrieve_screen"); }
+hipError_t launch_retrieve_decide(const RetrieveParams&, hipStream_t) {
+  return reached("retrieve_decide");
+}
+hipError_t launch_query_scan(const ScanParams&, const RetrieveParams&, int, int, hipStream_t) {
+  return reached("query_scan");
+}
 hipError_t launch_retrieve_prepare(const RetrieveParams&, hipStream_t) {
   return reached("retrieve_prepare");
 }

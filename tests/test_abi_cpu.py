@@ -160,6 +160,55 @@ def test_retrieve_validation_errors():
     assert call(Q=0) == OK
 
 
+def _query(desc, q=FAKE, K=FAKE, prepared=None, pbytes=0, M=100, E=64, store=FAKE, idx=FAKE,
+           x=FAKE, y=FAKE, hT=FAKE, ws=FAKE, wsb=None):
+    d = desc if desc is None else ctypes.byref(desc)
+    if wsb is None:
+        wsb = P.query_workspace_bytes(desc, M, E) if desc is not None else 0
+    return P.lib().precog_query_top1_prefill(d, q, K, prepared, pbytes, M, E, store, idx, x, FAKE,
+                                             FAKE, FAKE, FAKE, FAKE, FAKE, y, hT, ws, wsb, None)
+
+
+def test_query_call_validation_errors():
+    """precog_query_top1_prefill checks every argument of both halves (the
+    retrieval and the prefill from the store) before the device."""
+    good = P.scan_desc(8, 16, 64, 16, P.BF16, P.BF16, P.F16)
+    assert _query(None) == ENULL
+    assert _query(good, q=None) == ENULL
+    assert _query(good, idx=None) == ENULL
+    assert _query(good, K=None) == ENULL
+    assert _query(good, store=None) == ENULL        # M > 0 rows need a store
+    assert _query(good, x=None) == ENULL             # the prefill's inputs
+    assert _query(good, E=6) == EALIGN
+    assert _query(good, E=2) == ESHAPE
+    assert _query(good, M=-1) == ESHAPE
+    assert _query(good, q=FAKE + 4) == EALIGN
+    assert _query(good, store=FAKE + 8) == EALIGN
+    assert _query(good, hT=FAKE + 2) == EALIGN
+    assert _query(good, ws=None) == EWS
+    assert _query(good, wsb=P.retrieve_workspace_bytes(8, 100, 64) - 1) == EWS
+    assert _query(good, prepared=FAKE, pbytes=P.retrieve_index_bytes(100, 64) - 1) == EWS
+    assert _query(P.scan_desc(8, 16, 64, 16, P.F16)) == EDTYPE
+    assert _query(P.scan_desc(8, 16, 60, 16)) == EALIGN
+    assert _query(P.scan_desc(8, 16, 64, 3)) == ESHAPE
+    # time chunks need the scan's workspace after the retrieval's
+    few = P.scan_desc(2, 4096, 64, 16)
+    need = P.query_workspace_bytes(few, 100, 64)
+    assert need > P.retrieve_workspace_bytes(2, 100, 64) and P.scan_workspace_bytes(few) > 0
+    assert _query(few, wsb=need - 1) == EWS
+    # nothing to do: no queries
+    assert _query(P.scan_desc(0, 16, 64, 16), q=None, idx=None, ws=None, wsb=0) == OK
+
+
+def test_query_workspace_bytes():
+    desc = P.scan_desc(256, 32, 1024, 16, P.BF16, P.BF16, P.F16)
+    r = P.retrieve_workspace_bytes(256, 10000, 384)
+    assert P.query_workspace_bytes(desc, 10000, 384) == (r + 255) // 256 * 256
+    assert P.scan_workspace_bytes(desc) == 0  # 4096 waves: one pass
+    assert P.query_workspace_bytes(P.scan_desc(2, 16, 60, 16), 10, 64) == 0   # invalid desc
+    assert P.query_workspace_bytes(desc, 10, 6) == 0                         # invalid E
+
+
 def test_trajectory_validation_errors():
     L = P.lib()
     good = P.scan_desc(2, 16, 64, 16)
