@@ -780,8 +780,19 @@ __device__ __forceinline__ void scan_body(
   }
 }
 
+// The readout-free kinds over 16-bit inputs with N = 16 (the chunked scan's
+// summary pass, state-only encodes) are built for at most 128 VGPRs: four
+// waves per SIMD, two 512-thread workgroups per CU.  Left to itself the
+// compiler gave them 135-138, one workgroup per CU (two waves per SIMD) in
+// the many-round launches of the summary pass; at 128 it keeps a few values
+// that live across the time loop in scratch, none inside it.  Every other
+// instantiation keeps the compiler's own allocation.
+template <int N, typename TIn, int KIND, int TRAJ>
+constexpr int kScanMinWaves = (KIND != kReadout && TRAJ == 0 && N == 16 && sizeof(TIn) == 2) ? 4 : 1;
+
 template <int N, typename TIn, typename TOut, typename TSt, int KIND, bool HASZ, int TRAJ>
-__global__ __launch_bounds__(kSBlock) void scan_kernel(
+__global__ __launch_bounds__(kSBlock)
+__attribute__((amdgpu_waves_per_eu(kScanMinWaves<N, TIn, KIND, TRAJ>))) void scan_kernel(
     const TIn* __restrict__ xg, const TIn* __restrict__ dtg, const TIn* __restrict__ zg,
     const TIn* __restrict__ Bg, const TIn* __restrict__ Cg, TOut* __restrict__ yg,
     const ScanParams p) {
