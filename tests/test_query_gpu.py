@@ -185,3 +185,52 @@ def test_query_call_repeated_calls_deterministic():
     a = _one_call(desc, qd, Kd, store, d, torch.bfloat16, True, poison=False)
     b = _one_call(desc, qd, Kd, store, d, torch.bfloat16, True, poison=True)
     _assert_same(a, b)
+
+
+def _clustered(Q, M, E, spread, seed):
+    """Unit keys and queries around one direction: the smaller `spread`, the
+    more 32-key blocks come within the screen's error bound of the best."""
+    g = np.random.default_rng(seed)
+    base = g.standard_normal(E)
+    K = base[None, :] + spread * g.standard_normal((M, E))
+    K = (K / np.linalg.norm(K, axis=1, keepdims=True)).astype(np.float32)
+    q = base[None, :] + 0.3 * g.standard_normal((Q, E))
+    q = (q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32)
+    return torch.from_numpy(q), torch.from_numpy(K)
+
+
+def _check_heavy(q, K, L, D, seed, prepared):
+    Q, M = q.shape[0], K.shape[0]
+    store = synth.state_store(M, D * 16, seed=seed, device=DEV).view(M, D, 16)
+    inp = synth.scan_inputs_host(Q, L, D, 16, seed + 1, torch.bfloat16)
+    d = {k: v.to(DEV) for k, v in inp.items()}
+    qd, Kd = q.to(DEV), K.to(DEV)
+    prep = P.prepare_index(Kd) if prepared else None
+    desc = P.scan_desc(Q, L, D, 16, P.BF16, P.F32, P.F16, chunk=L)
+    a = _two_calls(desc, qd, Kd, store, d, torch.float32, True, prep)
+    b = _one_call(desc, qd, Kd, store, d, torch.float32, True, prep)
+    _assert_same(a, b)
+    ref_idx, _ = oracle.top1(q, K, nthreads=8)
+    assert np.array_equal(b[0].cpu().numpy(), ref_idx)
+
+
+@pytest.mark.parametrize("spread", [1e-3, 3e-2])
+def test_query_call_decision_past_the_register_groups(spread):
+    """The decision inside the one-launch path (one wave of a 512-thread
+    workgroup) with 40,000 keys = 1,250 blocks, past the 512 whose maxima it
+    holds in registers: every block survives at spread 1e-3 (every key a
+    candidate, the candidate list scored in many batches), some at 3e-2; then
+    one key of norm 1000 (every key scored exactly), prepared index too."""
+    q, K = _clustered(8, 40000, 64, spread, 65)
+    _check_heavy(q, K, 7, 64, 91, prepared=False)
+    K2 = K.clone()
+    K2[12345] *= 1000.0
+    _check_heavy(q, K2, 7, 64, 92, prepared=True)
+
+
+def test_query_call_largest_feature_count():
+    """E = 4096, the largest feature count (one candidate row per rescoring
+    batch), inside the one-launch path, unprepared and prepared."""
+    q, K, _, _ = synth.retrieval_inputs_host(40, 300, 4096, 3, seed=40 + 300 + 4096)
+    _check_heavy(q, K, 11, 192, 93, prepared=False)
+    _check_heavy(q, K, 11, 192, 94, prepared=True)
