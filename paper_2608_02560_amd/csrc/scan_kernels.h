@@ -854,6 +854,67 @@ __global__ __launch_bounds__(256) void carry_kernel(const ScanParams p, int N) {
   }
 }
 
+// Pass 2 for short sequences over few channels, where the fold's length
+// and not its bytes is the cost: one wave per (b, d, n), lane j holding the
+// step of chunk j, H -> m_j H + s_j with m_j = exp2(A' S_j), and an
+// inclusive scan of the steps over the lanes (composition (m, s) after
+// (m', s') = (m m', m s' + s); row shifts by 1, 2, 4, 8, then lane 15 of
+// rows 0 and 2 into rows 1 and 3, then lane 31 into rows 2 and 3), so every
+// carry needs one round trip instead of one per batch of chunks.  The same
+// carries as carry_kernel up to fp32 reassociation.
+constexpr int kCarryScanMaxChunks = 64;
+constexpr int64_t kCarryScanMaxLanes = 8192;  // (b, d, n) lanes: waves of strided loads
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void affine_step(float& m, float& s) {
+  // lanes without a source keep the identity step (1, 0)
+  const float mo = __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, 1.f), __builtin_bit_cast(int, m), CTRL,
+                                         ROWS, 0xf, false));
+  const float so = __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, 0.f), __builtin_bit_cast(int, s), CTRL,
+                                         ROWS, 0xf, false));
+  s = fmaf(m, so, s);
+  m = m * mo;
+}
+
+template <typename TSt>
+__global__ __launch_bounds__(256) void carry_scan_kernel(const ScanParams p, int N) {
+  const int64_t DN = p.D * N;
+  const int64_t w = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) >> 6;
+  if (w >= p.B * DN) return;  // whole waves
+  const int lane = threadIdx.x & 63;
+  const int64_t b = w / DN;
+  const int64_t dn = w - b * DN;
+  const int64_t d = dn / N;
+  const float a2 = -kLog2e * p.A[dn];
+  float H = 0.f;
+  if (p.h0_score != nullptr) {
+    float hv[1];
+    compose_state<1, TSt>(hv, p, b, dn);
+    H = hv[0];
+  } else if (p.flags & kHasH0) {
+    const TSt* src = h0_row<TSt>(p, b);
+    H = src != nullptr ? to_f32(src[dn]) : __builtin_nanf("");
+  }
+  float* cp = p.carry + b * p.nchunks * DN + dn;
+  const float* sp = p.dtsum + b * p.nchunks * p.D + d;
+  const bool on = lane < p.nchunks - 1;
+  float m = 1.f, s = 0.f;
+  if (on) {
+    s = cp[static_cast<int64_t>(lane + 1) * DN];
+    m = __builtin_amdgcn_exp2f(a2 * sp[static_cast<int64_t>(lane) * p.D]);
+  }
+  affine_step<0x111, 0xf>(m, s);  // row_shr:1
+  affine_step<0x112, 0xf>(m, s);  // row_shr:2
+  affine_step<0x114, 0xf>(m, s);  // row_shr:4
+  affine_step<0x118, 0xf>(m, s);  // row_shr:8
+  affine_step<0x142, 0xa>(m, s);  // row_bcast:15
+  affine_step<0x143, 0xc>(m, s);  // row_bcast:31
+  if (on) cp[static_cast<int64_t>(lane + 1) * DN] = fmaf(m, H, s);
+  if (lane == 0) cp[0] = H;
+}
+
 // The final pass: readout (with or without gate) or state-only, with the
 // trajectory mode TRAJ (0 none, 1 direct stores, 2 stores transposed
 // through LDS).
@@ -886,8 +947,12 @@ hipError_t launch_typed(const ScanParams& p, hipStream_t s) {
                        static_cast<const TIn*>(p.z), static_cast<const TIn*>(p.Bm),
                        static_cast<const TIn*>(p.Cm), static_cast<float*>(nullptr), p);
     const int64_t lanes = p.B * p.D * N;
-    hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
-                       0, s, p, N);
+    if (p.nchunks > 8 && p.nchunks <= kCarryScanMaxChunks && lanes <= kCarryScanMaxLanes)
+      hipLaunchKernelGGL((carry_scan_kernel<TSt>), dim3(static_cast<unsigned>((lanes * 64 + 255) / 256)),
+                         dim3(256), 0, s, p, N);
+    else
+      hipLaunchKernelGGL((carry_kernel<TSt>), dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
+                         0, s, p, N);
   }
   const int64_t g3 = rows_blocks * p.nchunks;
   if constexpr (!TRAJ) {

@@ -247,6 +247,63 @@ def test_chunk_sweep_agrees():
         assert err_rms(_np(hT), h_ref) <= 1e-5, chunk
 
 
+@pytest.mark.parametrize("B,L,D,N,chunk", [(1, 512, 128, 16, 0), (2, 500, 64, 16, 56),
+                                           (2, 500, 64, 16, 16), (3, 300, 40, 16, 5),
+                                           (1, 640, 8, 64, 10), (1, 190, 8, 2, 3)])
+@pytest.mark.parametrize("sd", [torch.float32, torch.float16])
+def test_short_sequence_carries(B, L, D, N, chunk, sd):
+    """9 to 64 time chunks over at most 8192 (b, d, n) lanes, where the
+    carries come from a scan over the chunks' steps (one wave per lane)
+    instead of the sequential fold: the automatic choice for the single
+    layer, ragged last chunks, channels past the last full wave, N = 64 and
+    N = 2; from a nonzero initial state in fp32 and fp16, against the oracle
+    (fp32 bar; an fp16 hT within one fp16 ulp)."""
+    inp = synth.scan_inputs_host(B, L, D, N, seed=B * 7 + L + D + N, in_dtype=torch.float32)
+    h0 = torch.from_numpy(np.random.default_rng(L).normal(0, 0.5, (B, D, N))).to(sd)
+    d = _dev(inp)
+    y, hT = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0.to(DEV),
+                   state_dtype=sd, chunk=chunk)
+    torch.cuda.synchronize()
+    y_ref, h_ref = _full_oracle(inp, h0.double().numpy())
+    assert err_rms(_np(y), y_ref) <= TOL_F32
+    if sd == torch.float32:
+        assert err_rms(_np(hT), h_ref) <= TOL_F32
+    else:
+        assert _f16_ulp_ok(hT, h_ref)
+
+
+def test_short_sequence_carries_from_store():
+    """The chunk-step scan with the injected start read inside it: from
+    store[idx[b]] and from a softmax composition of k rows, bitwise those of
+    gather (compose) + scan in the same chunks; an index outside the store
+    gives a NaN row."""
+    B, L, D, N, M = 3, 300, 64, 16, 12
+    inp = synth.scan_inputs_host(B, L, D, N, seed=79, in_dtype=torch.float32)
+    d = _dev(inp)
+    store = torch.from_numpy(np.random.default_rng(12).normal(0, 0.5, (M, D, N))).float().to(DEV)
+    idx = torch.tensor([5, -1, 11], dtype=torch.int32, device=DEV)
+    y, hT = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx, d["C"], d["z"],
+                              d["Dskip"], chunk=16)
+    h0 = P.gather(store.view(M, D * N), idx, out_dtype=torch.float32).view(B, D, N)
+    y2, h2 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0, chunk=16)
+    idx3 = torch.tensor([[1, 2, 3], [4, 12, 5], [0, 0, 1]], dtype=torch.int32, device=DEV)
+    sc = torch.tensor([[0.3, 0.2, 0.25], [0.1, 0.2, 0.3], [0.5, 0.5, 0.1]], dtype=torch.float64,
+                      device=DEV)
+    y3, h3 = P.scan_from_store(d["x"], d["dt"], d["A"], d["B"], store, idx3, d["C"], d["z"],
+                               d["Dskip"], score=sc, tau=0.1, chunk=16)
+    hc = P.compose(store.view(M, D * N), idx3, sc, tau=0.1, out_dtype=torch.float32).view(B, D, N)
+    y4, h4 = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=hc, chunk=16)
+    torch.cuda.synchronize()
+    ok = torch.tensor([True, False, True])
+    for a, b in ((y, y2), (hT, h2), (y3, y4), (h3, h4)):
+        assert torch.equal(a[ok], b[ok])
+        assert torch.isnan(a[~ok]).all() and torch.isnan(b[~ok]).all()
+    y_ref, h_ref = _full_oracle({k: (v[[0, 2]] if v.dim() == 3 else v) for k, v in inp.items()},
+                                store.cpu().double().numpy()[[5, 11]])
+    assert err_rms(_np(y[[0, 2]]), y_ref) <= TOL_F32
+    assert err_rms(_np(hT[[0, 2]]), h_ref) <= TOL_F32
+
+
 # ---------------------------------------------------------------------------
 # Workload-sized runs, sampled rows
 # ---------------------------------------------------------------------------
