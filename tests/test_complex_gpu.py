@@ -18,6 +18,10 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
 def _dev(inp):
     return {k: (v.to(DEV) if v is not None else None) for k, v in inp.items()}
 
@@ -149,21 +153,32 @@ def test_complex_chunked_state_only_and_h0_stride():
     assert not torch.any(hTs[:, 2 * D * N:])  # nothing written past each row
 
 
-def test_complex_chunked_zero_frequency_equals_real_chunked_scan():
+@pytest.mark.parametrize("chunk", [100, 64])
+def test_complex_chunked_zero_frequency_equals_real_chunked_scan(chunk):
     """w = 0: the chunked complex scan performs the real chunked scan's fp32
-    operations (summary, fold with cos 0 = 1 and sin 0 = 0, replay), so with
-    the same chunks y and Re hT are bitwise equal and Im hT is zero."""
+    operations (summary, sequential fold with cos 0 = 1 and sin 0 = 0,
+    replay), so where the real scan folds its 7 chunks sequentially too, y
+    and Re hT are bitwise equal; with 11 chunks over 8192 (b, d, n) lanes
+    the real scan composes the chunk steps by a scan over the chunks
+    instead, the same carries up to fp32 reassociation (the composition of
+    the chunks' affine maps is associative), so there the two agree within
+    the fp32 bar.  Im hT is zero either way."""
     inp = synth.scan_inputs_host(2, 700, 256, 16, seed=505, in_dtype=torch.bfloat16)
     d = _dev(inp)
     h0r = torch.from_numpy(np.random.default_rng(506).normal(0, 0.5, (2, 256, 16))).float().to(DEV)
     h0c = torch.stack([h0r, torch.zeros_like(h0r)], dim=-1).contiguous()
     y_c, h_c = P.scan_complex(d["x"], d["dt"], d["A"], torch.zeros_like(d["A"]), d["B"], d["C"],
-                              d["z"], d["Dskip"], h0c, chunk=64)
+                              d["z"], d["Dskip"], h0c, chunk=chunk)
     y_r, h_r = P.scan(d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"], d["Dskip"], h0=h0r,
-                      chunk=64)
+                      chunk=chunk)
     torch.cuda.synchronize()
-    assert torch.equal(y_c, y_r)
-    assert torch.equal(h_c[..., 0], h_r) and not torch.any(h_c[..., 1])
+    assert not torch.any(h_c[..., 1])
+    if chunk == 100:
+        assert torch.equal(y_c, y_r)
+        assert torch.equal(h_c[..., 0], h_r)
+    else:
+        assert err_rms(_np(y_c), _np(y_r)) <= TOL_F32
+        assert err_rms(_np(h_c[..., 0]), _np(h_r)) <= TOL_F32
 
 
 def test_complex_long_context_sampled_and_chunk_sweep():
