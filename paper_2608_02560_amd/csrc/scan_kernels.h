@@ -23,8 +23,10 @@
 //       pass 1 (summary): each chunk except the last is scanned from a zero
 //              state; its end state and sum of dt are written to workspace;
 //       pass 2 (carry):   per (b, d, n), H_c = exp(-A sum dt_{c-1}) H_{c-1}
-//              + s_{c-1}, sequential over chunks (the composition of the
-//              affine maps h -> a h + s that each chunk applies, App. A);
+//              + s_{c-1} (the composition of the affine maps h -> a h + s
+//              that each chunk applies, App. A): sequential over chunks, or
+//              for 9 to 64 chunks over few lanes a scan over the chunks'
+//              maps within one wave;
 //       pass 3 (replay):  each chunk is rescanned from its carried-in state,
 //              producing y and, for the last chunk, hT.
 //     The carried state is exact up to fp32 reassociation (Theorem 1 applied
