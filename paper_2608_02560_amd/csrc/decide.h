@@ -425,6 +425,9 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
       int best_i = -1;
       for (int c0 = 0; c0 < ncand; c0 += batch_max) {
         const int nb = ncand - c0 < batch_max ? ncand - c0 : batch_max;
+        // the batch's squared norms, one lane each, in flight with its rows
+        // (the list is complete: test_list ended with a wave_sync)
+        const float cn2 = lane < nb ? p.rownorm2[cand[c0 + lane]] : 0.f;
         stage_rows(c0, nb);
         for (int r = 0; r < nb; ++r) {
           const float* row = rs + r * pitch;
@@ -433,7 +436,8 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
             part = fma(qs[e], static_cast<double>(row[e]), part);
           const double a = wave_sum_d(part);
           const int ci = cand[c0 + r];
-          const double mu = gs * qn * sqrt(static_cast<double>(p.rownorm2[ci])) + 1e-300;
+          const float n2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cn2), r));
+          const double mu = gs * qn * sqrt(static_cast<double>(n2)) + 1e-300;
           if (best_i < 0 || a > best || (a == best && ci < best_i)) {
             if (best_i >= 0) others = fmax(others, best + best_mu);
             best = a;
