@@ -189,30 +189,55 @@ template <> struct V8<f16_t> {
 // Workgroup (slice, r): state row r, elements [2048 slice, 2048 slice + 2048).
 // The row slice is loaded once, every chunk routed to r is applied in chunk
 // order in registers, and the slice is stored once, so states are read and
-// written once and each contribution is read once.  Each update is
-// s' = fma(alpha, h, (1 - alpha) s) in fp32 with both factors rounded once
-// from fp64 (alpha = 1 gives s' = h exactly); fp16 states are rounded to
-// nearest even after every update, as an fp16 store would be.
+// written once and each contribution is read once.  The targets are read 64
+// at a time, one per lane (in flight with the state row), and a ballot gives
+// the chunks routed to r in order; their contributions are loaded
+// kEmaBatch at a time before the batch is applied in chunk order.  Each
+// update is s' = fma(alpha, h, (1 - alpha) s) in fp32 with both factors
+// rounded once from fp64 (alpha = 1 gives s' = h exactly); fp16 states are
+// rounded to nearest even after every update, as an fp16 store would be.
+constexpr int kEmaBatch = 4;
+
 template <typename TS, typename TH>
 __global__ __launch_bounds__(256) void ema_kernel(const EmaParams p) {
   const int64_t r = blockIdx.y;
   const int64_t e = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
-  if (e >= p.S) return;
+  // whole waves past the row end leave; lanes past it stay for the ballots
+  if (e - static_cast<int64_t>(threadIdx.x & 63) * 8 >= p.S) return;
+  const bool live = e < p.S;
+  const int lane = static_cast<int>(threadIdx.x & 63);
   const float a = p.alpha;
   const float b = p.one_minus_alpha;
   const int64_t so = r * p.S + e;
-  float8 s = V8<TS>::load(p.states, so);
+  float8 s = {};
+  if (live) s = V8<TS>::load(p.states, so);
   bool touched = false;
-  for (int64_t c = 0; c < p.C; ++c) {
-    if (p.target[c] != r) continue;  // wave-uniform: same chunk list for all lanes
-    const float8 h = V8<TH>::load(p.contrib, c * p.S + e);
+  for (int64_t c0 = 0; c0 < p.C; c0 += 64) {
+    const int64_t ci = c0 + lane;
+    uint64_t m = __ballot(ci < p.C && p.target[ci] == r);
+    while (m) {
+      int64_t cb[kEmaBatch];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) s[k] = fmaf(a, h[k], b * s[k]);
-    if constexpr (std::is_same<TS, f16_t>::value)
-      s = __builtin_convertvector(__builtin_convertvector(s, half8), float8);
-    touched = true;
+      for (int j = 0; j < kEmaBatch; ++j) {
+        cb[j] = m ? c0 + __builtin_ctzll(m) : -1;
+        m &= m - 1;
+      }
+      float8 h[kEmaBatch];
+#pragma unroll
+      for (int j = 0; j < kEmaBatch; ++j)
+        if (cb[j] >= 0 && live) h[j] = V8<TH>::load(p.contrib, cb[j] * p.S + e);
+#pragma unroll
+      for (int j = 0; j < kEmaBatch; ++j) {
+        if (cb[j] < 0) break;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) s[k] = fmaf(a, h[j][k], b * s[k]);
+        if constexpr (std::is_same<TS, f16_t>::value)
+          s = __builtin_convertvector(__builtin_convertvector(s, half8), float8);
+      }
+      touched = true;
+    }
   }
-  if (touched) V8<TS>::store(p.states, so, s);
+  if (touched && live) V8<TS>::store(p.states, so, s);
 }
 
 }  // namespace
