@@ -183,8 +183,15 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
   const double qn = static_cast<double>(qnorm);
   const double gq = p.err_g * qn + p.err_h;
   const double hq = p.err_h * qn + p.err_tiny;
-  // error bound of a screen score whose key has squared norm <= n2
-  auto err = [&](float n2) { return gq * sqrt(static_cast<double>(n2)) + hq; };
+  // error bound of a screen score whose key has squared norm <= n2.  The
+  // root is the fp32 one (v_sqrt_f32, within 1 ulp) of n2 raised to at
+  // least the smallest normal, widened by 2^-16 in fp64: never below the
+  // true root, so the bound stays an upper bound (the tests only ever pass
+  // more keys), without an fp64 root per block (NaN stays NaN)
+  auto err = [&](float n2) {
+    const float r = __builtin_amdgcn_sqrtf(n2 < 0x1p-126f ? 0x1p-126f : n2);
+    return gq * (static_cast<double>(r) * (1.0 + 0x1p-16)) + hq;
+  };
   const bool exhaustive = !(qnorm2 < kMaxNorm2) || !(nmax < kMaxNorm2);
   const double thresh = exhaustive ? -INFINITY : static_cast<double>(tk) - err(nmax);
 
