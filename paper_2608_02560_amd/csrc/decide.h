@@ -74,6 +74,9 @@ __device__ __forceinline__ void wave_sync() {
 // into a rank list spread over the lanes (lane j holds rank j), ordered by
 // score, then by lower index; the order of the batches does not change the
 // list.
+// FL: row loads in flight per round when a whole block is rescored in fp32
+// (as many as the caller's register budget allows).
+template <int FL>
 __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t q,
                                                 DecideShared& sh) {
   const int lane = threadIdx.x & 63;
@@ -344,19 +347,27 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
         const bool kok = r < cnt;
         float part[4] = {0.f, 0.f, 0.f, 0.f};
         if (kok) {
+          // FL 16-byte loads of the row in flight per round (the sum's
+          // order is free: any order stays within gamma_{E+1})
           const float4* row = reinterpret_cast<const float4*>(p.K + (b0 + r) * p.E);
-          for (int e4 = lane >> 5; e4 < e4n; e4 += 8) {
+          for (int e0 = lane >> 5; e0 < e4n; e0 += 2 * FL) {
+            float4 v[FL];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int f = e4 + 2 * u;
+            for (int u = 0; u < FL; ++u) {
+              const int f = e0 + 2 * u;
+              v[u] = f < e4n ? row[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < FL; ++u) {
+              const int f = e0 + 2 * u;
               if (f < e4n) {
-                const float4 v = row[f];
                 const double2 q01 = *reinterpret_cast<const double2*>(qs + 4 * f);
                 const double2 q23 = *reinterpret_cast<const double2*>(qs + 4 * f + 2);
-                part[u] = fmaf(static_cast<float>(q01.x), v.x, part[u]);
-                part[u] = fmaf(static_cast<float>(q01.y), v.y, part[u]);
-                part[u] = fmaf(static_cast<float>(q23.x), v.z, part[u]);
-                part[u] = fmaf(static_cast<float>(q23.y), v.w, part[u]);
+                float& a = part[u & 3];
+                a = fmaf(static_cast<float>(q01.x), v[u].x, a);
+                a = fmaf(static_cast<float>(q01.y), v[u].y, a);
+                a = fmaf(static_cast<float>(q23.x), v[u].z, a);
+                a = fmaf(static_cast<float>(q23.y), v[u].w, a);
               }
             }
           }

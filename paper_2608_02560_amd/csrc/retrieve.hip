@@ -361,7 +361,7 @@ __global__ __launch_bounds__(64) void prep_norms_kernel(const RetrieveParams p) 
 
 __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   __shared__ DecideShared sh;
-  decide_query(p, blockIdx.x, sh);
+  decide_query<16>(p, blockIdx.x, sh);
 }
 
 }  // namespace

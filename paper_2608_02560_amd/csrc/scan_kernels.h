@@ -741,7 +741,7 @@ __device__ __forceinline__ void scan_body(
     __shared__ DecideShared dsh;
     __shared__ int32_t dec_row;
     if (wave == 0) {
-      const int32_t r = decide_query(*rp, b, dsh);
+      const int32_t r = decide_query<6>(*rp, b, dsh);
       if (lane == 0) dec_row = r;
     }
     __syncthreads();
