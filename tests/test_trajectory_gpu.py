@@ -28,7 +28,9 @@ def _ref_traj(inp, every, h0=None):
 @pytest.mark.parametrize("B,L,D,N,every,chunk", [
     (2, 64, 64, 16, 1, 0), (2, 64, 64, 16, 5, 0), (1, 96, 136, 16, 7, 32),
     (3, 50, 72, 64, 4, 0), (2, 77, 64, 64, 10, 20), (2, 40, 16, 4, 3, 0),
-    (1, 33, 64, 16, 33, 0), (1, 33, 64, 16, 40, 0)])
+    (1, 33, 64, 16, 33, 0), (1, 33, 64, 16, 40, 0),
+    # 9 to 64 chunks over few (b, d, n): carries from the scan over the chunks' steps
+    (1, 300, 64, 16, 3, 0), (2, 200, 64, 64, 5, 16)])
 def test_trajectory_fp32(B, L, D, N, every, chunk):
     inp = synth.scan_inputs_host(B, L, D, N, seed=B * 100 + L + N, in_dtype=torch.float32)
     h0 = torch.from_numpy(np.random.default_rng(L).normal(0, 0.5, (B, D, N))).float()
