@@ -242,3 +242,35 @@ def test_scan_from_store_k1_scores_equal_plain_index():
                                d["C"], d["z"], d["Dskip"])
     torch.cuda.synchronize()
     assert torch.equal(y, y2) and torch.equal(hT, h2)
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_topk_keys_and_queries_of_mixed_norms(k):
+    """Keys with norms spread over 1e-3 .. 200 (squared norms below the
+    screen's overflow limit, so the per-block and per-key error bounds of the
+    decision decide) and queries with norms 1e-2 .. 50: indices and fp64
+    scores bit-exact, unprepared and with the prepared index; top-1 also
+    through the one-call query path."""
+    g = np.random.default_rng(97)
+    q, K, _, _ = synth.retrieval_inputs_host(96, 3000, 256, 8, seed=97)
+    Kn = K.numpy() * np.exp(g.uniform(np.log(1e-3), np.log(200.0), (3000, 1))).astype(np.float32)
+    qn = q.numpy() * np.exp(g.uniform(np.log(1e-2), np.log(50.0), (96, 1))).astype(np.float32)
+    q2, K2 = torch.from_numpy(qn.astype(np.float32)), torch.from_numpy(Kn.astype(np.float32))
+    assert float((K2.double() ** 2).sum(1).max()) < 60000.0
+    _check_topk(q2, K2, k)
+    qd, Kd = q2.to(DEV), K2.to(DEV)
+    prep = P.prepare_index(Kd)
+    i1, s1 = P.topk_prepared(qd, Kd, prep, k)
+    torch.cuda.synchronize()
+    ref_i, ref_s = oracle.topk_scores(q2, K2, k)
+    assert np.array_equal(i1.cpu().numpy(), ref_i.astype(np.int32))
+    assert np.array_equal(s1.cpu().numpy(), ref_s)
+    if k == 1:
+        D, L = 64, 5
+        store = synth.state_store(3000, D * 16, seed=98, device=DEV).view(3000, D, 16)
+        inp = synth.scan_inputs_host(96, L, D, 16, 99, torch.bfloat16)
+        d = {key: v.to(DEV) for key, v in inp.items()}
+        idx, _, _ = P.query_prefill(qd, Kd, store, d["x"], d["dt"], d["A"], d["B"], d["C"], d["z"],
+                                    d["Dskip"], chunk=L)
+        torch.cuda.synchronize()
+        assert np.array_equal(idx.cpu().numpy(), ref_i[:, 0].astype(np.int32))
