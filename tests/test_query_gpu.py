@@ -100,7 +100,7 @@ def test_query_call_workload_matches_two_calls_and_oracle(prepared):
     assert err_rms(b[2].double().cpu().numpy(), h_ref) <= TOL_BF16
 
 
-@pytest.mark.parametrize("Q,M,E,L,D", [(37, 1000, 64, 23, 1000), (3, 33, 16, 1, 520),
+@pytest.mark.parametrize("Q,M,E,L,D", [(37, 1000, 64, 23, 1000), (3, 33, 16, 1, 520), (520, 900, 96, 6, 64),
                                        (70, 4099, 388, 40, 64), (1, 1, 4, 9, 8)])
 @pytest.mark.parametrize("sd", [torch.float16, torch.float32])
 def test_query_call_ragged_one_pass(Q, M, E, L, D, sd):

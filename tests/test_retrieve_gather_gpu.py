@@ -33,7 +33,8 @@ def test_retrieval_workload_bit_exact():
 
 
 @pytest.mark.parametrize("Q,M,E", [(1, 1, 4), (3, 33, 16), (65, 1000, 20), (70, 97, 388),
-                                   (130, 4099, 64), (8, 20000, 1024), (5, 70001, 8)])
+                                   (130, 4099, 64), (8, 20000, 1024), (5, 70001, 8),
+                                   (300, 2000, 128), (5000, 700, 64)])
 def test_retrieval_ragged_shapes(Q, M, E):
     q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 4), seed=Q * 7 + M + E)
     ref, _ = oracle.top1(q, K, nthreads=8)

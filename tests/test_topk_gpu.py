@@ -56,7 +56,8 @@ def test_topk_survivors_past_the_register_groups(spread):
 
 
 @pytest.mark.parametrize("Q,M,E,k", [(1, 1, 4, 1), (3, 33, 16, 2), (65, 1000, 20, 5),
-                                     (70, 97, 388, 64), (130, 300, 64, 7), (5, 64, 8, 64)])
+                                     (70, 97, 388, 64), (130, 300, 64, 7), (5, 64, 8, 64),
+                                     (600, 1500, 96, 3)])
 def test_topk_ragged_shapes(Q, M, E, k):
     q, K, _, _ = synth.retrieval_inputs_host(Q, M, E, min(Q, 4), seed=Q * 5 + M + E + k)
     _check_topk(q, K, k)
