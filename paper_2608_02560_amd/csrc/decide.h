@@ -41,10 +41,12 @@ constexpr float kMaxNorm2 = 60000.f;
 constexpr int kRowWords = 8192;       // LDS words for staged candidate rows
 constexpr int kCacheGroups = 2;       // 256-block groups whose maxima stay in registers
 
-// LDS of one deciding wave.
+// LDS of one deciding wave.  The query in fp64 takes the first E doubles
+// of `qr`; the staged candidate rows take the rest (so a short query leaves
+// room for more rows per batch: 40 rows of 384 features instead of 21).
+constexpr int kQRWords = 2 * kMaxE + kRowWords;  // 4-byte words of `qr`
 struct DecideShared {
-  double qs[kMaxE] __attribute__((aligned(16)));   // the query in fp64 (exact)
-  float rs[kRowWords] __attribute__((aligned(16))); // staged candidate rows
+  float qr[kQRWords] __attribute__((aligned(16)));
   int cand[kCand];
   int blist[kBList];
   double slot_s[64];
@@ -83,8 +85,11 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
   const int E = static_cast<int>(p.E);
   const int nkb = p.nkb;
   const int k = p.k;
-  double* const qs = sh.qs;
-  float* const rs = sh.rs;
+  // the query (exact in fp64) first, the staged rows after it; E is a
+  // multiple of 4, so the rows stay 16-byte aligned
+  double* const qs = reinterpret_cast<double*>(sh.qr);
+  float* const rs = sh.qr + 2 * E;
+  const int row_words = kQRWords - 2 * E;
   int* const cand = sh.cand;
   int* const blist = sh.blist;
   double* const slot_s = sh.slot_s;
@@ -245,7 +250,7 @@ __device__ __forceinline__ int32_t decide_query(const RetrieveParams& p, int64_t
   // exact scores of the listed candidates, a batch of rows at a time
   const int pitch = E + 4;  // E is a multiple of 4: rows stay 16-byte aligned
   const uint64_t inv_e4n = ((1ull << 32) + static_cast<uint64_t>(e4n) - 1) / static_cast<uint64_t>(e4n);
-  const int batch_max = kRowWords / pitch < 64 ? kRowWords / pitch : 64;
+  const int batch_max = row_words / pitch < 64 ? row_words / pitch : 64;
   int ncand = 0;
   bool early = false;  // a batch was scored before the list was complete
   // rows cand[c0 .. c0 + nb) into rs (row pitch `pitch`): one flat
