@@ -359,9 +359,13 @@ __global__ __launch_bounds__(64) void prep_norms_kernel(const RetrieveParams p) 
   if (lane == 0) p.blocknorm2[kb] = mx;
 }
 
+// FL: row loads in flight when a whole block is rescored.  Top-1 keeps 16
+// (24 took its decision from 7.1 to 7.5 us: more registers on its short
+// path); top-k, which rescores whole blocks more often, takes 24.
+template <int FL>
 __global__ __launch_bounds__(64) void decide_kernel(const RetrieveParams p) {
   __shared__ DecideShared sh;
-  decide_query<16>(p, blockIdx.x, sh);
+  decide_query<FL>(p, blockIdx.x, sh);
 }
 
 }  // namespace
@@ -416,7 +420,10 @@ hipError_t launch_retrieve_screen(RetrieveParams& p, hipStream_t s) {
 }
 
 hipError_t launch_retrieve_decide(const RetrieveParams& p, hipStream_t s) {
-  hipLaunchKernelGGL(decide_kernel, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
+  if (p.k == 1)
+    hipLaunchKernelGGL(decide_kernel<16>, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
+  else
+    hipLaunchKernelGGL(decide_kernel<24>, dim3(static_cast<unsigned>(p.Q)), dim3(64), 0, s, p);
   return hipGetLastError();
 }
 
